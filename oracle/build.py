@@ -1,0 +1,33 @@
+"""Compile the CPU oracle (plain C) into oracle/liboracle.so.
+
+Test infrastructure: only the tests, the smoke check and the benchmark's
+CPU-baseline leg load the result.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB = os.path.join(HERE, "liboracle.so")
+
+
+def build(verbose: bool = False, src: str | None = None, out: str | None = None) -> str:
+    """Compile `src` (default: the oracle) into `out` (default: oracle/liboracle.so)."""
+    src = src or os.path.join(HERE, "deamoe_oracle.c")
+    lib = out or LIB
+    # -ffp-contract=off: no fused multiply-add, every product and sum rounds
+    # separately; no fast-math, so exp and division are the C library's.
+    cmd = ["gcc", "-std=gnu11", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+           "-fPIC", "-shared", "-Wall", "-Wextra", "-Wno-unused-parameter",
+           "-I", HERE, "-o", lib + ".tmp", src, "-lm"]
+    if verbose:
+        print(" ".join(cmd), file=sys.stderr)
+    subprocess.run(cmd, check=True)
+    os.replace(lib + ".tmp", lib)
+    return lib
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))
