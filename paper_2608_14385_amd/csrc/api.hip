@@ -1,0 +1,471 @@
+// Host side of the C ABI: validation, workspace layout and the launch
+// sequence of one decode step.  Nothing here allocates, frees or waits.
+#include <string.h>
+
+#include <algorithm>
+
+#include "gemm_tile.h"
+#include "launch.h"
+
+using namespace deamoe;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int kstep_of(int w_dtype) { return w_dtype == DEAMOE_F32 ? 64 : 128; }
+int wbytes_of(int w_dtype) { return w_dtype == DEAMOE_F32 ? 4 : w_dtype == DEAMOE_BF16 ? 2 : 1; }
+int abytes_of(int act_dtype) { return act_dtype == DEAMOE_F32 ? 4 : 2; }
+
+// Number of hidden-dimension chunks the router product is split into: the
+// largest divisor of the K steps that keeps >= 4 steps per chunk (one per
+// wave) and about 256 workgroups in total.
+int router_chunks(const deamoe_config &c) {
+  const int ks = c.act_dtype == DEAMOE_F32 ? 64 : 128;
+  const int steps = c.hidden / ks;
+  const int tiles = (c.n_experts + kTile - 1) / kTile;
+  const int want = (256 + tiles - 1) / tiles;
+  int best = 1;
+  for (int d = 1; d <= steps; ++d)
+    if (steps % d == 0 && d <= want && steps / d >= 4) best = d;
+  return best;
+}
+
+int max_slots_of(const deamoe_config &c) { return 2 * c.top_k + 1; }
+
+bool has_private(const deamoe_config &c) {
+  return c.form == DEAMOE_FORM_FACTORED || c.d_private > 0;
+}
+
+struct Layout {
+  size_t logits, part, topk_ids, topk_w, tok_depts, tok_dept_w, tok_ndept, dept_count,
+      dept_offset, dept_tokens, exp_count, exp_offset, exp_tokens;
+  size_t counts, units[kMaxStages], slot_pair, slot_w, nslot, tok_exp_pair, exp_src;
+  size_t abuf_dept, abuf_exp, abuf_se, gbuf, ubuf, ybuf, zbuf, zsbuf, partial;
+  size_t total;
+  int kc, max_units, max_dept_pairs, max_exp_pairs;
+};
+
+Layout make_layout(const deamoe_config &c) {
+  Layout L;
+  const size_t T = (size_t)c.max_tokens, n = c.n_experts, m = c.n_depts, k = c.top_k;
+  const size_t h = c.hidden, ab = abytes_of(c.act_dtype);
+  const size_t dk = std::min<size_t>(c.top_k_dept > 0 ? c.top_k_dept : k, std::min(k, m));
+  L.kc = router_chunks(c);
+  L.max_units = (int)(m + n + 1);
+  L.max_dept_pairs = (int)(T * dk);
+  L.max_exp_pairs = (int)(T * k);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + (bytes ? bytes : 1));
+    return o;
+  };
+  L.logits = take(T * n * 4);
+  L.part = take((size_t)L.kc * T * n * 4);
+  L.topk_ids = take(T * k * 4);
+  L.topk_w = take(T * k * 4);
+  L.tok_depts = take(T * k * 4);
+  L.tok_dept_w = take(T * k * 4);
+  L.tok_ndept = take(T * 4);
+  L.dept_count = take(m * 4);
+  L.dept_offset = take((m + 1) * 4);
+  L.dept_tokens = take(T * k * 4);
+  L.exp_count = take(n * 4);
+  L.exp_offset = take((n + 1) * 4);
+  L.exp_tokens = take(T * k * 4);
+  L.counts = take(sizeof(PlanCounts));
+  for (int s = 0; s < kMaxStages; ++s) L.units[s] = take((size_t)L.max_units * sizeof(GemmUnit));
+  const size_t S = max_slots_of(c);
+  L.slot_pair = take(T * S * 4);
+  L.slot_w = take(T * S * 4);
+  L.nslot = take(T * 4);
+  L.tok_exp_pair = take(T * k * 4);
+  L.exp_src = take(T * k * 4);
+  const size_t dpairs = L.max_dept_pairs, epairs = L.max_exp_pairs;
+  const size_t ds = c.d_shared, dp = c.d_private, dse = c.d_shared_expert;
+  L.abuf_se = take(T * dse * ab);
+  if (c.form == DEAMOE_FORM_SLICE) {
+    L.abuf_dept = take(dpairs * ds * ab);
+    L.abuf_exp = take(epairs * dp * ab);
+    L.gbuf = L.ubuf = L.ybuf = L.zbuf = L.zsbuf = 0;
+    L.partial = take((dpairs + (dp ? epairs : 0) + (dse ? T : 0)) * h * 4);
+  } else {
+    L.abuf_dept = L.abuf_exp = 0;
+    L.gbuf = take(dpairs * ds * ab);
+    L.ubuf = take(dpairs * ds * ab);
+    L.ybuf = take(epairs * ds * ab);
+    L.zbuf = take(epairs * ds * 4);
+    L.zsbuf = take(dpairs * ds * ab);
+    L.partial = take((dpairs + (dse ? T : 0)) * h * 4);
+  }
+  L.total = off;
+  return L;
+}
+
+int validate_config(const deamoe_config *c) {
+  if (!c) return DEAMOE_ERR_INVALID;
+  if (c->hidden <= 0 || c->n_experts <= 0 || c->n_depts <= 0) return DEAMOE_ERR_INVALID;
+  if (c->n_experts % c->n_depts) return DEAMOE_ERR_INVALID;
+  if (c->top_k <= 0 || c->top_k > c->n_experts) return DEAMOE_ERR_INVALID;
+  if (c->top_k_dept < 0 || c->top_k_dept > c->n_depts) return DEAMOE_ERR_INVALID;
+  const int E = c->n_experts / c->n_depts;
+  if (c->top_k_dept > 0 && c->top_k > c->top_k_dept * E) return DEAMOE_ERR_INVALID;
+  if (c->d_shared <= 0 || c->d_private < 0 || c->d_shared_expert < 0) return DEAMOE_ERR_INVALID;
+  if (c->form != DEAMOE_FORM_SLICE && c->form != DEAMOE_FORM_FACTORED) return DEAMOE_ERR_INVALID;
+  if (c->score != DEAMOE_SCORE_SOFTMAX && c->score != DEAMOE_SCORE_SIGMOID) return DEAMOE_ERR_INVALID;
+  if (c->renorm != 0 && c->renorm != 1) return DEAMOE_ERR_INVALID;
+  if (c->sigma != DEAMOE_SIGMA_SILU && c->sigma != DEAMOE_SIGMA_NONE) return DEAMOE_ERR_INVALID;
+  if (!(c->route_scale == c->route_scale)) return DEAMOE_ERR_INVALID;
+  if (c->w_dtype < DEAMOE_F32 || c->w_dtype > DEAMOE_FP8_E4M3_B128) return DEAMOE_ERR_INVALID;
+  if (c->act_dtype != DEAMOE_F32 && c->act_dtype != DEAMOE_BF16) return DEAMOE_ERR_INVALID;
+  if (c->max_tokens <= 0) return DEAMOE_ERR_INVALID;
+  // limits of this build
+  if (c->max_tokens > DEAMOE_MAX_TOKENS || c->n_experts > DEAMOE_MAX_EXPERTS ||
+      c->top_k > DEAMOE_MAX_TOPK || c->n_depts > kMaxM)
+    return DEAMOE_ERR_UNSUPPORTED;
+  if (c->top_k_dept > 0 && c->n_depts > kMaxMGrouped) return DEAMOE_ERR_UNSUPPORTED;
+  // fp32 weights pair with fp32 activations, bf16 / fp8 weights with bf16
+  if ((c->w_dtype == DEAMOE_F32) != (c->act_dtype == DEAMOE_F32)) return DEAMOE_ERR_UNSUPPORTED;
+  // every contraction length is a whole number of matrix-core K steps
+  const int ks = kstep_of(c->w_dtype);
+  if (c->hidden % ks || c->d_shared % ks) return DEAMOE_ERR_UNSUPPORTED;
+  if (c->form == DEAMOE_FORM_SLICE && c->d_private % ks) return DEAMOE_ERR_UNSUPPORTED;
+  if (c->d_shared_expert % ks) return DEAMOE_ERR_UNSUPPORTED;
+  return DEAMOE_OK;
+}
+
+int validate_weights(const deamoe_config &c, const deamoe_weights *w, bool need_router) {
+  if (!w) return DEAMOE_ERR_INVALID;
+  if (need_router && !w->router) return DEAMOE_ERR_INVALID;
+  const void *mats[9] = {w->dept_gate, w->dept_up, w->dept_down, w->priv_gate, w->priv_up,
+                         w->priv_down, w->se_gate, w->se_up, w->se_down};
+  bool used[9] = {true, true, true, has_private(c), has_private(c), has_private(c),
+                  c.d_shared_expert > 0, c.d_shared_expert > 0, c.d_shared_expert > 0};
+  for (int i = 0; i < 9; ++i) {
+    if (!used[i]) continue;
+    if (!mats[i] || ((uintptr_t)mats[i] & 15)) return DEAMOE_ERR_INVALID;
+    if (c.w_dtype == DEAMOE_FP8_E4M3_B128 && (!w->scale[i] || ((uintptr_t)w->scale[i] & 3)))
+      return DEAMOE_ERR_INVALID;
+  }
+  if (w->router && ((uintptr_t)w->router & 15)) return DEAMOE_ERR_INVALID;
+  return DEAMOE_OK;
+}
+
+int ntt_of(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
+
+template <class P>
+P *at(void *ws, size_t off) {
+  return reinterpret_cast<P *>(static_cast<char *>(ws) + off);
+}
+
+struct Events {
+  void *const *ev;
+  int n, next;
+  hipStream_t s;
+  hipError_t mark() {
+    if (!ev || next >= n) return hipSuccess;
+    return hipEventRecord(static_cast<hipEvent_t>(ev[next++]), s);
+  }
+};
+
+int check(hipError_t e) { return e == hipSuccess ? DEAMOE_OK : DEAMOE_ERR_HIP; }
+
+#define DEAMOE_TRY(expr)                    \
+  do {                                      \
+    const int _rc = check(expr);            \
+    if (_rc != DEAMOE_OK) return _rc;       \
+  } while (0)
+
+// Router product and route/plan kernels.
+int enqueue_route(const deamoe_config &c, int T, const void *x, const void *router_w,
+                  const float *logits_in, const float *bias, const deamoe_routing &r, void *ws,
+                  const Layout &L, int plan, const deamoe_weights *w, Events &ev,
+                  hipStream_t s) {
+  DEAMOE_TRY(ev.mark());
+  RouteArgs a;
+  memset(&a, 0, sizeof a);
+  if (!logits_in) {
+    RouterArgs ra;
+    ra.w = router_w;
+    ra.x = x;
+    ra.part = at<float>(ws, L.part);
+    ra.n = c.n_experts;
+    ra.h = c.hidden;
+    ra.T = T;
+    ra.kchunk = c.hidden / L.kc;
+    ra.tiles = (c.n_experts + kTile - 1) / kTile;
+    DEAMOE_TRY(launch_router(ra, c.act_dtype == DEAMOE_F32 ? WT_F32 : WT_BF16, ntt_of(T), L.kc, s));
+    DEAMOE_TRY(ev.mark());
+  }
+  a.T = T;
+  a.n = c.n_experts;
+  a.m = c.n_depts;
+  a.k = c.top_k;
+  a.kdept = c.top_k_dept;
+  a.E = c.n_experts / c.n_depts;
+  a.score = c.score;
+  a.renorm = c.renorm;
+  a.route_scale = c.route_scale;
+  a.h = c.hidden;
+  a.d_s = c.d_shared;
+  a.d_p = c.form == DEAMOE_FORM_SLICE ? c.d_private : 0;
+  a.d_se = c.d_shared_expert;
+  a.act_f32 = c.act_dtype == DEAMOE_F32;
+  a.w_bytes = wbytes_of(c.w_dtype);
+  a.fp8 = c.w_dtype == DEAMOE_FP8_E4M3_B128;
+  a.plan = plan;
+  a.part = at<float>(ws, L.part);
+  a.kc = L.kc;
+  a.logits_in = logits_in;
+  a.bias = bias;
+  a.r = r;
+  a.counts = at<PlanCounts>(ws, L.counts);
+  for (int i = 0; i < kMaxStages; ++i) a.units[i] = at<GemmUnit>(ws, L.units[i]);
+  a.slot_pair = at<int32_t>(ws, L.slot_pair);
+  a.nslot = at<int32_t>(ws, L.nslot);
+  a.slot_w = at<float>(ws, L.slot_w);
+  a.tok_exp_pair = at<int32_t>(ws, L.tok_exp_pair);
+  a.exp_src = at<int32_t>(ws, L.exp_src);
+  a.max_slots = max_slots_of(c);
+  if (w) a.w = *w;
+  a.x = x;
+  a.abuf_dept = at<void>(ws, L.abuf_dept);
+  a.abuf_exp = at<void>(ws, L.abuf_exp);
+  a.abuf_se = at<void>(ws, L.abuf_se);
+  a.gbuf = at<void>(ws, L.gbuf);
+  a.ubuf = at<void>(ws, L.ubuf);
+  a.ybuf = at<void>(ws, L.ybuf);
+  a.zsbuf = at<void>(ws, L.zsbuf);
+  a.zbuf = at<float>(ws, L.zbuf);
+  a.partial = at<float>(ws, L.partial);
+  DEAMOE_TRY(launch_route_plan(a, s));
+  DEAMOE_TRY(ev.mark());
+  return DEAMOE_OK;
+}
+
+deamoe_routing routing_in_ws(void *ws, const Layout &L, const deamoe_routing *user) {
+  deamoe_routing r;
+  if (user) {
+    r = *user;
+  } else {
+    r.topk_ids = at<int32_t>(ws, L.topk_ids);
+    r.topk_w = at<float>(ws, L.topk_w);
+    r.tok_depts = at<int32_t>(ws, L.tok_depts);
+    r.tok_dept_w = at<float>(ws, L.tok_dept_w);
+    r.tok_ndept = at<int32_t>(ws, L.tok_ndept);
+    r.dept_count = at<int32_t>(ws, L.dept_count);
+    r.dept_offset = at<int32_t>(ws, L.dept_offset);
+    r.dept_tokens = at<int32_t>(ws, L.dept_tokens);
+    r.exp_count = at<int32_t>(ws, L.exp_count);
+    r.exp_offset = at<int32_t>(ws, L.exp_offset);
+    r.exp_tokens = at<int32_t>(ws, L.exp_tokens);
+    r.logits = nullptr;
+  }
+  if (!r.logits) r.logits = at<float>(ws, L.logits);
+  return r;
+}
+
+bool routing_complete(const deamoe_routing &r) {
+  return r.topk_ids && r.topk_w && r.tok_depts && r.tok_dept_w && r.tok_ndept && r.dept_count &&
+         r.dept_offset && r.dept_tokens && r.exp_count && r.exp_offset && r.exp_tokens;
+}
+
+// Upper bound of the row tiles of a stage, for the grid size.
+int tiles_bound(int units_max, int R) { return units_max * ((R + kTile - 1) / kTile); }
+
+constexpr int kGridCap = 2048;   // 256 CUs x 8 workgroups
+
+int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_weights *w,
+               const float *logits_in, const float *bias, deamoe_routing *routing_out, void *y,
+               void *ws, size_t ws_bytes, void *stream, void *const *events, int32_t n_events) {
+  int rc = validate_config(cfg);
+  if (rc) return rc;
+  const deamoe_config &c = *cfg;
+  if (T < 0 || T > c.max_tokens) return T < 0 ? DEAMOE_ERR_INVALID : DEAMOE_ERR_UNSUPPORTED;
+  if ((rc = validate_weights(c, w, !logits_in))) return rc;
+  if (!x || !y) return DEAMOE_ERR_INVALID;
+  if (routing_out && !routing_complete(*routing_out)) return DEAMOE_ERR_INVALID;
+  if (n_events < 0 || (n_events > 0 && !events)) return DEAMOE_ERR_INVALID;
+  const Layout L = make_layout(c);
+  if (!ws || ws_bytes < L.total) return DEAMOE_ERR_WORKSPACE;
+  if ((uintptr_t)ws % kAlign) return DEAMOE_ERR_WORKSPACE;
+  if (T == 0) return DEAMOE_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Events ev{events, n_events, 0, s};
+  const deamoe_routing r = routing_in_ws(ws, L, routing_out);
+  const bool slice = c.form == DEAMOE_FORM_SLICE;
+  rc = enqueue_route(c, T, x, w->router, logits_in, bias, r, ws, L,
+                     slice ? PLAN_SLICE : PLAN_FACTORED, w, ev, s);
+  if (rc) return rc;
+  const int wt = c.w_dtype == DEAMOE_F32 ? WT_F32 : c.w_dtype == DEAMOE_BF16 ? WT_BF16 : WT_FP8;
+  const int ntt = ntt_of(T);
+  const PlanCounts *pc = at<PlanCounts>(ws, L.counts);
+  auto stage = [&](int i) {
+    GemmStage st;
+    st.units = at<GemmUnit>(ws, L.units[i]);
+    st.counts = pc->stage[i];
+    st.sigma = c.sigma;
+    return st;
+  };
+  const int m = c.n_depts, dk = L.max_dept_pairs / c.max_tokens;
+  const int act_depts = std::min(m, T * dk);
+  const int act_exps = std::min(c.n_experts, T * c.top_k);
+  const int se = c.d_shared_expert > 0 ? 1 : 0;
+  if (slice) {
+    const int ta = tiles_bound(act_depts, c.d_shared) +
+                   (c.d_private ? tiles_bound(act_exps, c.d_private) : 0) +
+                   se * tiles_bound(1, c.d_shared_expert);
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, ntt, 4, ta, kGridCap, s));
+    DEAMOE_TRY(ev.mark());
+    const int units = act_depts + (c.d_private ? act_exps : 0) + se;
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 1, ntt, 1, tiles_bound(units, c.hidden), kGridCap, s));
+    DEAMOE_TRY(ev.mark());
+  } else {
+    const int d = c.d_shared;
+    const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, ntt, 4, t0, kGridCap, s));
+    DEAMOE_TRY(ev.mark());
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, ntt, 4, tiles_bound(act_exps, d), kGridCap, s));
+    DEAMOE_TRY(ev.mark());
+    DEAMOE_TRY(launch_grouped_gemm(stage(2), wt, 1, ntt, 4, tiles_bound(act_exps, d), kGridCap, s));
+    DEAMOE_TRY(ev.mark());
+    ZsumArgs za;
+    za.counts = pc;
+    za.dept_tokens = r.dept_tokens;
+    za.dept_offset = r.dept_offset;
+    za.topk_ids = r.topk_ids;
+    za.tok_exp_pair = at<int32_t>(ws, L.tok_exp_pair);
+    za.topk_w = r.topk_w;
+    za.z = at<float>(ws, L.zbuf);
+    za.zs = at<void>(ws, L.zsbuf);
+    za.m = m;
+    za.k = c.top_k;
+    za.E = c.n_experts / m;
+    za.d = d;
+    za.act_f32 = c.act_dtype == DEAMOE_F32;
+    DEAMOE_TRY(launch_zsum(za, T * dk, s));
+    DEAMOE_TRY(ev.mark());
+    DEAMOE_TRY(launch_grouped_gemm(stage(3), wt, 1, ntt, 1, tiles_bound(act_depts + se, c.hidden),
+                                   kGridCap, s));
+    DEAMOE_TRY(ev.mark());
+  }
+  CombineArgs ca;
+  ca.partial = at<float>(ws, L.partial);
+  ca.slot_pair = at<int32_t>(ws, L.slot_pair);
+  ca.nslot = at<int32_t>(ws, L.nslot);
+  ca.slot_w = at<float>(ws, L.slot_w);
+  ca.y = y;
+  ca.T = T;
+  ca.h = c.hidden;
+  ca.max_slots = max_slots_of(c);
+  ca.act_f32 = c.act_dtype == DEAMOE_F32;
+  DEAMOE_TRY(launch_combine(ca, s));
+  DEAMOE_TRY(ev.mark());
+  return DEAMOE_OK;
+}
+
+int64_t matrix_bytes(int w_dtype, int64_t R, int64_t C) {
+  int64_t b = R * C * wbytes_of(w_dtype);
+  if (w_dtype == DEAMOE_FP8_E4M3_B128) b += ((R + 127) / 128) * ((C + 127) / 128) * 4;
+  return b;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *deamoe_status_string(int status) {
+  switch (status) {
+    case DEAMOE_OK: return "ok";
+    case DEAMOE_ERR_INVALID: return "invalid argument";
+    case DEAMOE_ERR_UNSUPPORTED: return "unsupported by this build";
+    case DEAMOE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case DEAMOE_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+int deamoe_workspace_bytes(const deamoe_config *cfg, size_t *bytes) {
+  const int rc = validate_config(cfg);
+  if (rc) return rc;
+  if (!bytes) return DEAMOE_ERR_INVALID;
+  *bytes = make_layout(*cfg).total;
+  return DEAMOE_OK;
+}
+
+int deamoe_route(const deamoe_config *cfg, int32_t T, const void *x, const void *router_w,
+                 const float *logits_in, const float *router_bias, deamoe_routing *out, void *ws,
+                 size_t ws_bytes, void *stream) {
+  int rc = validate_config(cfg);
+  if (rc) return rc;
+  const deamoe_config &c = *cfg;
+  if (T < 0) return DEAMOE_ERR_INVALID;
+  if (T > c.max_tokens) return DEAMOE_ERR_UNSUPPORTED;
+  if (!out || !routing_complete(*out)) return DEAMOE_ERR_INVALID;
+  if (!logits_in && (!x || !router_w)) return DEAMOE_ERR_INVALID;
+  if (router_w && ((uintptr_t)router_w & 15)) return DEAMOE_ERR_INVALID;
+  const Layout L = make_layout(c);
+  if (!ws || ws_bytes < L.total || (uintptr_t)ws % kAlign) return DEAMOE_ERR_WORKSPACE;
+  if (T == 0) return DEAMOE_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Events ev{nullptr, 0, 0, s};
+  const deamoe_routing r = routing_in_ws(ws, L, out);
+  return enqueue_route(c, T, x, router_w, logits_in, router_bias, r, ws, L, PLAN_NONE, nullptr,
+                       ev, s);
+}
+
+int deamoe_layer_forward(const deamoe_config *cfg, int32_t T, const void *x,
+                         const deamoe_weights *w, const float *logits_in,
+                         const float *router_bias, deamoe_routing *routing_out, void *y, void *ws,
+                         size_t ws_bytes, void *stream) {
+  return layer_impl(cfg, T, x, w, logits_in, router_bias, routing_out, y, ws, ws_bytes, stream,
+                    nullptr, 0);
+}
+
+int deamoe_layer_forward_traced(const deamoe_config *cfg, int32_t T, const void *x,
+                                const deamoe_weights *w, const float *logits_in,
+                                const float *router_bias, deamoe_routing *routing_out, void *y,
+                                void *ws, size_t ws_bytes, void *stream, void *const *events,
+                                int32_t n_events) {
+  return layer_impl(cfg, T, x, w, logits_in, router_bias, routing_out, y, ws, ws_bytes, stream,
+                    events, n_events);
+}
+
+int deamoe_baseline_forward(const deamoe_config *cfg, int32_t T, const void *x,
+                            const deamoe_weights *w, const float *logits_in,
+                            const float *router_bias, deamoe_routing *routing_out, void *y,
+                            void *ws, size_t ws_bytes, void *stream) {
+  if (!cfg) return DEAMOE_ERR_INVALID;
+  if (cfg->n_depts != cfg->n_experts || cfg->d_private != 0 || cfg->form != DEAMOE_FORM_SLICE ||
+      cfg->top_k_dept != 0)
+    return DEAMOE_ERR_INVALID;
+  return layer_impl(cfg, T, x, w, logits_in, router_bias, routing_out, y, ws, ws_bytes, stream,
+                    nullptr, 0);
+}
+
+int deamoe_loaded_bytes(const deamoe_config *cfg, int32_t T, const int32_t *dept_count,
+                        const int32_t *exp_count, int64_t *weight_bytes, int64_t *total_bytes) {
+  const int rc = validate_config(cfg);
+  if (rc) return rc;
+  if (T < 0 || !dept_count || !exp_count) return DEAMOE_ERR_INVALID;
+  const deamoe_config &c = *cfg;
+  const int64_t h = c.hidden, d = c.d_shared, p = c.d_private, e = c.d_shared_expert;
+  const int wt = c.w_dtype;
+  const int64_t ab = abytes_of(c.act_dtype);
+  int64_t dept = 3 * matrix_bytes(wt, d, h);
+  int64_t priv = 0;
+  if (c.form == DEAMOE_FORM_FACTORED) priv = 3 * matrix_bytes(wt, d, d);
+  else if (p > 0) priv = 3 * matrix_bytes(wt, p, h);
+  int64_t b = (int64_t)c.n_experts * h * ab;
+  for (int j = 0; j < c.n_depts; ++j) b += dept_count[j] > 0 ? dept : 0;
+  for (int i = 0; i < c.n_experts; ++i) b += exp_count[i] > 0 ? priv : 0;
+  if (e > 0) b += 3 * matrix_bytes(wt, e, h);
+  if (weight_bytes) *weight_bytes = b;
+  if (total_bytes) *total_bytes = b + 2 * (int64_t)T * h * ab;
+  return DEAMOE_OK;
+}
+
+}  // extern "C"

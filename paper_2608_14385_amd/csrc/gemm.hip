@@ -1,0 +1,83 @@
+// Grouped skinny GEMM over a device-built list of units (one launch per
+// stage).  The number of units and row tiles is only known on the device, so
+// the grid is fixed on the host and every workgroup walks tiles
+// blockIdx.x * TPB, + gridDim.x * TPB, ...; tiles past the end do nothing.
+#include "gemm_tile.h"
+#include "launch.h"
+
+namespace deamoe {
+
+constexpr int kMaxUnitsCached = 4096;
+
+template <int WT, int NW, int NTT, int KS>
+__global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
+  using Run = TileRunner<WT, NW, NTT, KS>;
+  __shared__ typename Run::Smem sm;
+  __shared__ int32_t s_begin[kMaxUnitsCached];
+  const int n_units = st.counts[0], n_tiles = st.counts[1];
+  for (int u = threadIdx.x; u < n_units; u += blockDim.x) s_begin[u] = st.units[u].tile_begin;
+  __syncthreads();
+  const int wave = threadIdx.x / kWave;
+  for (int base = blockIdx.x * Run::TPB; base < n_tiles; base += gridDim.x * Run::TPB) {
+    const int tile = base + wave / KS;
+    const bool active = tile < n_tiles;
+    int u = 0;
+    if (active) {  // last unit whose first tile is <= tile
+      int lo = 0, hi = n_units - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_begin[mid] <= tile) lo = mid; else hi = mid - 1;
+      }
+      u = lo;
+    }
+    const GemmUnit *U = st.units + u;
+    Run::run(sm, U, active ? tile - s_begin[u] : 0, active, st.sigma);
+  }
+}
+
+template <int WT, int NW, int NTT, int KS>
+static hipError_t launch_gemm(const GemmStage &st, int max_tiles, int grid_cap, hipStream_t s) {
+  constexpr int TPB = 4 / KS;
+  int grid = (max_tiles + TPB - 1) / TPB;
+  grid = grid < 1 ? 1 : (grid > grid_cap ? grid_cap : grid);
+  hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS>), dim3(grid), dim3(256), 0, s, st);
+  return hipGetLastError();
+}
+
+template <int WT, int NW, int KS>
+static hipError_t dispatch_ntt(const GemmStage &st, int ntt, int max_tiles, int cap, hipStream_t s) {
+  switch (ntt) {
+    case 1: return launch_gemm<WT, NW, 1, KS>(st, max_tiles, cap, s);
+    case 2: return launch_gemm<WT, NW, 2, KS>(st, max_tiles, cap, s);
+    case 4: return launch_gemm<WT, NW, 4, KS>(st, max_tiles, cap, s);
+    default: return launch_gemm<WT, NW, 8, KS>(st, max_tiles, cap, s);
+  }
+}
+
+template <int WT, int NW>
+static hipError_t dispatch_ks(const GemmStage &st, int ntt, int ks, int max_tiles, int cap,
+                              hipStream_t s) {
+  switch (ks) {
+    case 1: return dispatch_ntt<WT, NW, 1>(st, ntt, max_tiles, cap, s);
+    case 2: return dispatch_ntt<WT, NW, 2>(st, ntt, max_tiles, cap, s);
+    default: return dispatch_ntt<WT, NW, 4>(st, ntt, max_tiles, cap, s);
+  }
+}
+
+hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int ntt, int ks,
+                               int max_tiles, int grid_cap, hipStream_t s) {
+  if (nw == 2) {
+    switch (wtype) {
+      case WT_F32: return dispatch_ks<WT_F32, 2>(st, ntt, ks, max_tiles, grid_cap, s);
+      case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, ntt, ks, max_tiles, grid_cap, s);
+      default: return dispatch_ks<WT_FP8, 2>(st, ntt, ks, max_tiles, grid_cap, s);
+    }
+  }
+  switch (wtype) {
+    case WT_F32: return dispatch_ks<WT_F32, 1>(st, ntt, ks, max_tiles, grid_cap, s);
+    case WT_BF16: return dispatch_ks<WT_BF16, 1>(st, ntt, ks, max_tiles, grid_cap, s);
+    default: return dispatch_ks<WT_FP8, 1>(st, ntt, ks, max_tiles, grid_cap, s);
+  }
+}
+
+}  // namespace deamoe

@@ -1,0 +1,76 @@
+// Kernel argument blocks and host-side launchers shared by the library's
+// translation units.
+#pragma once
+
+#include "internal.h"
+
+namespace deamoe {
+
+constexpr int kRouteThreads = 1024;
+constexpr int kMaxT = DEAMOE_MAX_TOKENS;
+constexpr int kMaxK = DEAMOE_MAX_TOPK;
+constexpr int kMaxTK = kMaxT * kMaxK;
+constexpr int kMaxN = DEAMOE_MAX_EXPERTS;
+constexpr int kMaxM = 1024;
+constexpr int kMaxMGrouped = 64;   // departments when top_k_dept > 0
+
+// Router product: logits partial sums over KC chunks of the hidden dimension.
+struct RouterArgs {
+  const void *w;        // [n, h] act dtype
+  const void *x;        // [T, h] act dtype
+  float *part;          // [kc, T, n]
+  int32_t n, h, T, kchunk, tiles;
+};
+
+enum PlanMode : int32_t { PLAN_NONE = 0, PLAN_SLICE = 1, PLAN_FACTORED = 2 };
+
+struct RouteArgs {
+  // configuration
+  int32_t T, n, m, k, kdept, E, score, renorm;
+  float route_scale;
+  int32_t h, d_s, d_p, d_se, act_f32, w_bytes, fp8, plan;
+  // logits: sum of kc partial products, or injected; optional bias
+  const float *part;
+  int32_t kc;
+  const float *logits_in, *bias;
+  // routing outputs
+  deamoe_routing r;
+  // plan outputs
+  PlanCounts *counts;
+  GemmUnit *units[kMaxStages];
+  int32_t *slot_pair, *nslot, *tok_exp_pair, *exp_src;
+  float *slot_w;
+  int32_t max_slots;
+  // inputs of the planned stages
+  deamoe_weights w;
+  const void *x;
+  void *abuf_dept, *abuf_exp, *abuf_se;      // SLICE gate/up outputs
+  void *gbuf, *ubuf, *ybuf, *zsbuf;           // FACTORED intermediates (act dtype)
+  float *zbuf;                                // FACTORED sigma(A_d^T Y), fp32
+  float *partial;                             // [pairs, h] fp32
+};
+
+struct CombineArgs {
+  const float *partial;
+  const int32_t *slot_pair, *nslot;
+  const float *slot_w;
+  void *y;
+  int32_t T, h, max_slots, act_f32;
+};
+
+struct ZsumArgs {
+  const PlanCounts *counts;
+  const int32_t *dept_tokens, *dept_offset, *topk_ids, *tok_exp_pair;
+  const float *topk_w, *z;
+  void *zs;
+  int32_t m, k, E, d, act_f32;
+};
+
+hipError_t launch_router(const RouterArgs &a, int wtype, int ntt, int kc, hipStream_t s);
+hipError_t launch_route_plan(const RouteArgs &a, hipStream_t s);
+hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int ntt, int ks,
+                               int max_tiles, int grid_cap, hipStream_t s);
+hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
+hipError_t launch_zsum(const ZsumArgs &a, int max_dept_pairs, hipStream_t s);
+
+}  // namespace deamoe

@@ -1,0 +1,170 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Routing is compared bit-exactly on inputs whose logits are exact in fp32
+whatever the summation order (gate-exact tokens and router) or injected;
+layer outputs within max|err| <= tol * max|ref| (fp32 1e-4, bf16 2e-2,
+fp8 6e-2).  Full-size layers are checked on sampled tokens.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+from gpu_util import Case, compare_outputs, compare_routing, sample_tokens, say  # noqa: E402
+from paper_2608_14385_amd import deamoe as D  # noqa: E402
+from paper_2608_14385_amd import workloads as W  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+P = W.PRESETS
+
+
+def small(**kw):
+    base = dict(name="small", hidden=256, n_experts=16, n_depts=4, top_k=2, d_shared=512,
+                d_private=64, score="softmax", renorm=True, w_dtype="f32", act_dtype="f32")
+    base.update(kw)
+    return W.LayerConfig(**base)
+
+
+def check_case(case: Case, tokens=None, baseline=False, exact_logits=True):
+    cfg, T = case.cfg, case.T
+    say(f"[gpu] {cfg.name} form={cfg.form} w={cfg.w_dtype} T={T} baseline={baseline} "
+        f"logits={'injected' if case.logits is not None else 'computed'} "
+        f"bias={case.bias is not None}")
+    y, rt, _ = case.run_gpu(baseline=baseline)
+    ref_r = case.route_oracle()
+    compare_routing(rt.host(), ref_r, T, cfg.top_k, exact_logits=exact_logits)
+    y_ref = case.run_oracle(tokens=tokens)
+    return compare_outputs(y, y_ref, cfg.w_dtype, rows=tokens)
+
+
+# ------------------------------------------------------------- small, full oracle
+
+@pytest.mark.parametrize("T", [1, 4, 5, 17, 33, 128])
+def test_tiny_f32_slice(T):
+    check_case(Case(P["tiny_f32"].layer, T, seed=T, max_tokens=128 if T > 64 else None))
+
+
+@pytest.mark.parametrize("variant", ["uniform_logits", "zipf_bias", "softmax_no_renorm",
+                                     "sigmoid", "sigmoid_no_renorm_scaled", "group_limited",
+                                     "shared_expert", "no_private"])
+def test_small_variants(variant):
+    T = 9
+    if variant == "uniform_logits":
+        case = Case(small(), 16, seed=1, logits="uniform")
+    elif variant == "zipf_bias":
+        case = Case(small(score="sigmoid"), T, seed=2, bias="zipf")
+    elif variant == "softmax_no_renorm":
+        case = Case(small(renorm=False), T, seed=3)
+    elif variant == "sigmoid":
+        case = Case(small(score="sigmoid"), T, seed=4)
+    elif variant == "sigmoid_no_renorm_scaled":
+        case = Case(small(score="sigmoid", renorm=False, route_scale=2.5), T, seed=5)
+    elif variant == "group_limited":
+        case = Case(small(n_experts=64, n_depts=8, top_k=6, top_k_dept=3), 21, seed=6)
+    elif variant == "shared_expert":
+        case = Case(small(d_shared_expert=192), T, seed=7)
+    else:
+        case = Case(small(d_private=0), T, seed=8)
+    check_case(case)
+
+
+@pytest.mark.parametrize("T", [1, 4, 19])
+def test_tiny_factored(T):
+    check_case(Case(P["tiny_factored"].layer, T, seed=10 + T))
+
+
+@pytest.mark.parametrize("variant", ["sigma_none", "identity_private", "group_limited_se"])
+def test_factored_variants(variant):
+    base = P["tiny_factored"].layer
+    if variant == "sigma_none":
+        case = Case(base.replace(sigma="none"), 7, seed=20)
+    elif variant == "identity_private":
+        case = Case(base, 7, seed=21, identity_private=True)
+    else:
+        case = Case(base.replace(n_experts=32, n_depts=4, top_k=5, top_k_dept=2,
+                                 d_shared_expert=128, score="sigmoid"), 11, seed=22)
+    check_case(case)
+
+
+@pytest.mark.parametrize("T", [1, 4, 40])
+def test_tiny_baseline(T):
+    cfg = P["tiny_f32"].baseline
+    check_case(Case(cfg, T, seed=30 + T), baseline=True)
+
+
+@pytest.mark.parametrize("T", [1, 4, 16])
+def test_7b_bf16(T):
+    check_case(Case(P["7b_bf16"].layer, T, seed=40 + T, logits="uniform"))
+
+
+def test_7b_bf16_baseline():
+    check_case(Case(P["7b_bf16"].baseline, 16, seed=45, logits="uniform"), baseline=True)
+
+
+# ------------------------------------------------------------ full size, sampled
+
+@pytest.mark.parametrize("T", [1, 16, 64, 128])
+def test_dsv3_bf16(T):
+    case = Case(P["dsv3_bf16"].layer, T, seed=50 + T, max_tokens=128 if T > 64 else None)
+    check_case(case, tokens=sample_tokens(T))
+
+
+def test_dsv3_skew_bias():
+    case = Case(P["dsv3_skew"].layer, 128, seed=60, bias="zipf", max_tokens=128)
+    check_case(case, tokens=sample_tokens(128))
+
+
+def test_dsv3_skew_gumbel():
+    case = Case(P["dsv3_skew"].layer, 96, seed=61, logits="gumbel", max_tokens=128)
+    check_case(case, tokens=sample_tokens(96))
+
+
+@pytest.mark.parametrize("T", [1, 32])
+def test_dsv3_fp8(T):
+    case = Case(P["dsv3_fp8"].layer, T, seed=70 + T)
+    check_case(case, tokens=sample_tokens(T))
+
+
+@pytest.mark.parametrize("T", [1, 16])
+def test_dsv3_factored(T):
+    case = Case(P["dsv3_factored"].layer, T, seed=80 + T)
+    check_case(case, tokens=sample_tokens(T, 2))
+
+
+def test_dsv3_baseline():
+    case = Case(P["dsv3_bf16"].baseline, 16, seed=90)
+    check_case(case, tokens=sample_tokens(16, 2), baseline=True)
+
+
+# ------------------------------------------------------------ properties
+
+def test_deterministic_and_route_only():
+    case = Case(P["dsv3_bf16"].layer, 33, seed=91)
+    say("[gpu] determinism dsv3_bf16 T=33")
+    y1, r1, layer = case.run_gpu()
+    y2, r2, _ = case.run_gpu()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    h1, h2 = r1.host(), r2.host()
+    for k in h1:
+        assert np.array_equal(h1[k], h2[k]), k
+    # the router alone gives the same routing
+    rt = D.Routing.alloc(case.cfg, case.T)
+    D.deamoe_route(layer.c, case.x, case.w["router"], rt, layer.ws)
+    torch.cuda.synchronize()
+    h3 = rt.host()
+    for k in h1:
+        assert np.array_equal(h1[k], h3[k]), k
+
+
+def test_empty_batch_is_a_no_op():
+    cfg = P["tiny_f32"].layer
+    w = W.make_weights(cfg, 0, device="cuda")
+    layer = D.Layer(cfg, w, 8)
+    x = torch.zeros(0, cfg.hidden, device="cuda")
+    y = torch.zeros(0, cfg.hidden, device="cuda")
+    layer(x, y=y)
+    torch.cuda.synchronize()
