@@ -1,0 +1,351 @@
+#!/usr/bin/env python3
+"""DeaMoE MoE-layer decode benchmark on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--batch T]
+
+A step is one pass of the whole layer (router product, route/plan, gate/up,
+down, combine) over one batch of T synthetic tokens, through the C ABI.
+Weights are resident in HBM before timing; every step uses the next of R
+identical weight copies (R * layer bytes >> 256 MB of last-level cache) and
+the next of 8 token batches, so no step is served from a cache that the
+previous one filled.  Prints one JSON line (stdout); progress goes to stderr.
+
+value = algorithmic HBM bytes of the steps / their time (GB/s), where the
+algorithmic bytes of a step are the weights of every department and expert
+its routing touched, the router, the shared expert, x read and y written
+(deamoe_loaded_bytes on the step's own routing counts).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer decode latency (µs) + achieved HBM GB/s, batch 1–64, vs vanilla MoE"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="dsv3_bf16")
+    ap.add_argument("--batch", type=int, default=16)
+    ap.add_argument("--sweep", default="1,2,4,8,16,32,64",
+                    help="comma-separated batches for the latency sweep ('' to skip)")
+    ap.add_argument("--sweep-steps", type=int, default=50)
+    ap.add_argument("--no-baseline", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--copies", type=int, default=0, help="weight copies (0: automatic)")
+    return ap.parse_args()
+
+
+class Hip:
+    """The few HIP runtime calls the benchmark needs for raw events."""
+
+    def __init__(self):
+        self.lib = C.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [C.c_void_p]
+
+    def event(self) -> int:
+        e = C.c_void_p()
+        assert self.lib.hipEventCreate(C.byref(e)) == 0
+        return e.value
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = C.c_float()
+        assert self.lib.hipEventElapsedTime(C.byref(ms), C.c_void_p(a), C.c_void_p(b)) == 0
+        return float(ms.value)
+
+    def destroy(self, e: int):
+        self.lib.hipEventDestroy(C.c_void_p(e))
+
+
+class LayerRun:
+    """R weight copies, token batches and workspace of one layer on the GPU."""
+
+    def __init__(self, cfg, max_tokens: int, copies: int, baseline: bool, seed=0):
+        import torch
+        from paper_2608_14385_amd import deamoe as D
+        from paper_2608_14385_amd import workloads as W
+        self.D, self.W, self.torch = D, W, torch
+        self.cfg, self.baseline = cfg, baseline
+        t0 = time.time()
+        w0 = W.make_weights(cfg, seed, device="cuda")
+        self.copies = [w0] + [{k: v.clone() for k, v in w0.items()} for _ in range(copies - 1)]
+        self.structs = [D.make_weights(w) for w in self.copies]
+        self.layer_bytes = sum(t.numel() * t.element_size() for t in w0.values())
+        self.c = D.make_config(cfg, max_tokens)
+        self.ws = D.alloc_workspace(self.c)
+        self.fn = D.lib().deamoe_baseline_forward if baseline else D.lib().deamoe_layer_forward
+        self.traced = D.lib().deamoe_layer_forward_traced
+        torch.cuda.synchronize()
+        log(f"[bench] {cfg.name}: {copies} copies x {self.layer_bytes / 1e9:.2f} GB generated "
+            f"in {time.time() - t0:.1f}s")
+        self.xs, self.y, self.T = [], None, 0
+
+    def set_batch(self, T: int, n_x: int = 8):
+        W, torch = self.W, self.torch
+        self.T = T
+        self.xs = [W.make_tokens(self.cfg, T, 100 + i, device="cuda") for i in range(n_x)]
+        self.y = torch.empty_like(self.xs[0])
+        # algorithmic bytes of every token batch from its own routing
+        self.bytes = []
+        for x in self.xs:
+            rt = self.D.Routing.alloc(self.cfg, T)
+            self.D.deamoe_layer_forward(self.c, x, self.structs[0], self.y, self.ws, routing=rt) \
+                if not self.baseline else \
+                self.D.deamoe_baseline_forward(self.c, x, self.structs[0], self.y, self.ws, routing=rt)
+            h = rt.host()
+            wb, tb = self.D.deamoe_loaded_bytes(self.c, T, h["dept_count"], h["exp_count"])
+            self.bytes.append((wb, tb, h["dept_count"], h["exp_count"]))
+        torch.cuda.synchronize()
+
+    def step(self, i: int):
+        x = self.xs[i % len(self.xs)]
+        W = self.structs[i % len(self.structs)]
+        s = self.torch.cuda.current_stream().cuda_stream
+        rc = self.fn(C.byref(self.c), self.T, x.data_ptr(), C.byref(W), None, None, None,
+                     self.y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), s)
+        if rc:
+            raise RuntimeError(f"layer call failed: {self.D.status_string(rc)}")
+
+    def step_bytes(self, i: int) -> int:
+        return self.bytes[i % len(self.xs)][1]
+
+    def time_direct(self, steps: int, warmup: int) -> float:
+        torch = self.torch
+        for i in range(warmup):
+            self.step(i)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(steps):
+            self.step(i)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    def time_graph(self, steps: int, warmup: int) -> float:
+        """Steps captured in one hipGraph (8 steps per graph), replayed."""
+        torch = self.torch
+        per = 8
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for i in range(per):
+                self.step(i)
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            for i in range(per):
+                self.step(i)
+        reps = max(1, math.ceil(steps / per))
+        for _ in range(max(1, warmup // per)):
+            g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / (reps * per)
+
+    def time_stages(self, hip: Hip, steps: int) -> list:
+        """Per-kernel durations (ms) from HIP events recorded between the
+        kernels on the launch stream; returns one list of durations per step."""
+        torch = self.torch
+        n_ev = 6 if self.cfg.form == "slice" else 9
+        evs = [[hip.event() for _ in range(n_ev)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        for i in range(steps):
+            x = self.xs[i % len(self.xs)]
+            W = self.structs[i % len(self.structs)]
+            arr = (C.c_void_p * n_ev)(*evs[i])
+            s = torch.cuda.current_stream().cuda_stream
+            rc = self.traced(C.byref(self.c), self.T, x.data_ptr(), C.byref(W), None, None, None,
+                             self.y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), s, arr, n_ev)
+            assert rc == 0, rc
+        torch.cuda.synchronize()
+        out = [[hip.elapsed_ms(e[q], e[q + 1]) for q in range(n_ev - 1)] for e in evs]
+        for e in evs:
+            for q in e:
+                hip.destroy(q)
+        return out
+
+
+def stage_names(form: str) -> list:
+    if form == "slice":
+        return ["router_gemv", "route_plan", "gate_up", "down", "combine"]
+    return ["router_gemv", "route_plan", "dept_gate_up", "priv_gate_up", "priv_down", "z_collect",
+            "dept_down", "combine"]
+
+
+def gate_up_bytes(cfg, T: int, dept_count, exp_count) -> int:
+    """Algorithmic bytes of the gate/up kernel: the gate and up matrices of
+    every touched department, expert and the shared expert, plus x."""
+    wb = {"f32": 4, "bf16": 2, "fp8": 1}[cfg.w_dtype]
+    ab = 4 if cfg.act_dtype == "f32" else 2
+    h = cfg.hidden
+
+    def mat(R, Cc):
+        b = R * Cc * wb
+        if cfg.w_dtype == "fp8":
+            b += -(-R // 128) * -(-Cc // 128) * 4
+        return b
+    nd = int((np.asarray(dept_count) > 0).sum())
+    ne = int((np.asarray(exp_count) > 0).sum())
+    b = nd * 2 * mat(cfg.d_shared, h) + T * h * ab
+    if cfg.form == "slice" and cfg.d_private > 0:
+        b += ne * 2 * mat(cfg.d_private, h)
+    if cfg.d_shared_expert > 0:
+        b += 2 * mat(cfg.d_shared_expert, h)
+    return b
+
+
+def cpu_baseline(run: LayerRun, T: int, step_bytes: float) -> dict:
+    import oracle
+    threads = oracle.num_threads()
+    n_tok = min(T, max(threads, 1))
+    x = run.xs[0].cpu()
+    hw = {k: v.cpu() for k, v in run.copies[0].items()}
+    t0 = time.perf_counter()
+    oracle.layer(run.cfg, x, hw, tokens=list(range(n_tok)))
+    dt = time.perf_counter() - t0
+    step_s = dt * T / n_tok
+    return {"value": step_bytes / step_s / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_tok} of the {T} tokens of one {run.cfg.name} step, "
+                      f"naive fp64 per-token per-expert loop, {dt:.2f}s, scaled to the step",
+            "seconds_per_step": step_s}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        log("bench.py measures one GPU: the DeaMoE decode layer runs on a single MI355X and this "
+            "build has no multi-GPU path; run with --gpus 1.")
+        sys.exit(2)
+    import torch
+    from paper_2608_14385_amd import deamoe as D
+    from paper_2608_14385_amd import workloads as W
+    D.lib()   # fails loudly when the HIP library is missing
+    torch.cuda.set_device(0)
+    wl = W.PRESETS[args.workload]
+    cfg, bcfg = wl.layer, wl.baseline
+    sweep = [int(s) for s in args.sweep.split(",") if s.strip()]
+    max_T = max([args.batch] + sweep)
+    hip = Hip()
+
+    def copies_for(nbytes):
+        if args.copies:
+            return args.copies
+        return max(2, math.ceil(4 * 256e6 / nbytes))
+
+    layer_bytes = sum(math.prod(s) for s in W.weight_shapes(cfg).values()) * \
+        {"f32": 4, "bf16": 2, "fp8": 1}[cfg.w_dtype]
+    run = LayerRun(cfg, max_T, copies_for(layer_bytes), baseline=False)
+    T = args.batch
+    run.set_batch(T)
+    step_bytes = [run.step_bytes(i) for i in range(args.steps)]
+    log(f"[bench] timing {cfg.name} T={T}: {args.warmup} warmup + {args.steps} steps")
+    ms = run.time_direct(args.steps, args.warmup)
+    gbps = sum(step_bytes) / (ms * 1e-3 * args.steps) / 1e9
+    result = {"metric": METRIC, "value": round(gbps, 1), "unit": "GB/s", "n_gpus": 1,
+              "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.w_dtype,
+              "data": "synthetic (seeded gaussian weights and tokens, resident in HBM)"}
+    result["config"] = {
+        "workload": f"{cfg.name}: DeepSeek-V3-shaped DeaMoE layer, SLICE form, h={cfg.hidden}, "
+                    f"{cfg.n_experts} experts in {cfg.n_depts} departments, top-{cfg.top_k} "
+                    f"{cfg.score}, department slice {cfg.d_shared} + private slice {cfg.d_private}, "
+                    f"{cfg.w_dtype} weights" if cfg.name.startswith("dsv3") else cfg.name,
+        "batch_tokens": T, "weight_copies": len(run.copies), "token_batches": len(run.xs),
+        "timing": "direct launches on one stream, torch.cuda events around all steps"}
+    result["latency_us"] = round(ms * 1e3, 2)
+    result["bytes_per_step"] = int(np.mean(step_bytes))
+    result["hbm_frac"] = round(gbps / HBM_PEAK_GBPS, 4)
+    log(f"[bench] {cfg.name} T={T}: {ms * 1e3:.1f} us/step, {gbps:.0f} GB/s")
+
+    if not args.no_graph:
+        gms = run.time_graph(args.steps, args.warmup)
+        result["graph"] = {"latency_us": round(gms * 1e3, 2),
+                           "GBps": round(sum(step_bytes) / (gms * 1e-3 * args.steps) / 1e9, 1)}
+        log(f"[bench] graph replay: {gms * 1e3:.1f} us/step")
+
+    # per-kernel durations (HIP events on the launch stream, same region shape)
+    stages = run.time_stages(hip, args.steps)
+    names = stage_names(cfg.form)
+    mean = np.mean(np.asarray(stages), axis=0)
+    result["kernels_us"] = {n: round(float(v) * 1e3, 2) for n, v in zip(names, mean)}
+    dom = names.index("gate_up" if cfg.form == "slice" else "dept_gate_up")
+    gu = [gate_up_bytes(cfg, T, b[2], b[3]) for b in run.bytes]
+    gu_bytes = float(np.mean([gu[i % len(gu)] for i in range(args.steps)]))
+    achieved = gu_bytes / (mean[dom] * 1e-3) / 1e9
+    result["roofline"] = {"kernel": "grouped_gemm_kernel (gate/up stage)", "bound": "hbm",
+                          "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                          "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                          "bytes_per_launch": int(gu_bytes),
+                          "avg_launch_us": round(float(mean[dom]) * 1e3, 2)}
+    log(f"[bench] kernels (us): {result['kernels_us']}")
+
+    # vanilla-MoE comparator and the batch sweep
+    sweep_rows = []
+    brun = None
+    if not args.no_baseline:
+        bbytes = sum(math.prod(s) for s in W.weight_shapes(bcfg).values()) * \
+            {"f32": 4, "bf16": 2, "fp8": 1}[bcfg.w_dtype]
+        brun = LayerRun(bcfg, max_T, copies_for(bbytes), baseline=True)
+    for Tb in sweep:
+        row = {"batch": Tb}
+        for name, r in (("deamoe", run), ("vanilla", brun)):
+            if r is None:
+                continue
+            r.set_batch(Tb)
+            k = args.sweep_steps
+            m = r.time_direct(k, max(5, k // 5))
+            by = float(np.mean([r.step_bytes(i) for i in range(k)]))
+            row[name] = {"latency_us": round(m * 1e3, 2), "bytes": int(by),
+                         "GBps": round(by / (m * 1e-3) / 1e9, 1)}
+            if not args.no_graph:
+                gm = r.time_graph(k, 8)
+                row[name]["graph_latency_us"] = round(gm * 1e3, 2)
+        if brun is not None:
+            row["speedup"] = round(row["vanilla"]["latency_us"] / row["deamoe"]["latency_us"], 3)
+            row["byte_ratio"] = round(row["deamoe"]["bytes"] / row["vanilla"]["bytes"], 4)
+        log(f"[bench] sweep {row}")
+        sweep_rows.append(row)
+    if sweep_rows:
+        result["sweep"] = sweep_rows
+        head = [r for r in sweep_rows if r["batch"] == T]
+        if head and "speedup" in head[0]:
+            result["speedup_vs_vanilla"] = head[0]["speedup"]
+
+    if not args.no_cpu:
+        run.set_batch(T)
+        result["cpu_baseline"] = cpu_baseline(run, T, float(np.mean(step_bytes)))
+        log(f"[bench] cpu oracle: {result['cpu_baseline']}")
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

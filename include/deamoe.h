@@ -28,7 +28,8 @@
  *   - Arguments are validated on the host before anything is enqueued; an
  *     invalid call returns a negative DEAMOE_ERR_* code and enqueues nothing.
  *     A launch failure returns DEAMOE_ERR_HIP.
- *   - T == 0 returns DEAMOE_OK and enqueues nothing.
+ *   - T == 0 returns DEAMOE_OK and enqueues nothing once the configuration
+ *     is valid (tensor pointers may then be NULL).
  *   - Identical inputs give bit-identical outputs (no atomics in any sum).
  *   - The library holds no state: calls on different streams are independent
  *     as long as each uses its own workspace and outputs.

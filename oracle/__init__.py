@@ -42,6 +42,7 @@ class _Routing(C.Structure):
 def _open(path: str):
     """Load an oracle build and declare its signatures."""
     L = C.CDLL(path)
+    L.oref_num_threads.restype = C.c_int
     L.oref_fp8_value.restype = C.c_double
     L.oref_fp8_value.argtypes = [C.c_uint8]
     L.oref_fp8_decode.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p]
@@ -178,6 +179,11 @@ def layer_two_stage(cfg, x, weights: dict, logits_in=None, bias=None) -> np.ndar
     if rc:
         raise ValueError("oracle rejected the configuration")
     return y
+
+
+def num_threads() -> int:
+    """Threads the oracle's token loop runs on."""
+    return int(lib().oref_num_threads())
 
 
 def fp8_decode(codes) -> np.ndarray:

@@ -25,8 +25,11 @@
 #include "deamoe_oracle.h"
 
 #include <math.h>
+#include <omp.h>
 #include <stdlib.h>
 #include <string.h>
+
+int oref_num_threads(void) { return omp_get_max_threads(); }
 
 /* ---------------------------------------------------------------- decoding */
 

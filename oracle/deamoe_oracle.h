@@ -66,6 +66,9 @@ typedef struct {
   int32_t *exp_count, *exp_offset, *exp_tokens;      /* [n], [n+1], [T*k]      */
 } oref_routing;
 
+/* Threads the token loops of oref_layer_naive may use (OpenMP). */
+int oref_num_threads(void);
+
 /* e4m3fn (OCP) code -> value. */
 double oref_fp8_value(uint8_t code);
 void oref_fp8_decode(const uint8_t *codes, size_t count, double *out);

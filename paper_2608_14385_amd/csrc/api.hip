@@ -285,6 +285,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
   if (rc) return rc;
   const deamoe_config &c = *cfg;
   if (T < 0 || T > c.max_tokens) return T < 0 ? DEAMOE_ERR_INVALID : DEAMOE_ERR_UNSUPPORTED;
+  if (T == 0) return DEAMOE_OK;   // empty batch: nothing to read or write
   if ((rc = validate_weights(c, w, !logits_in))) return rc;
   if (!x || !y) return DEAMOE_ERR_INVALID;
   if (routing_out && !routing_complete(*routing_out)) return DEAMOE_ERR_INVALID;
@@ -292,7 +293,6 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
   const Layout L = make_layout(c);
   if (!ws || ws_bytes < L.total) return DEAMOE_ERR_WORKSPACE;
   if ((uintptr_t)ws % kAlign) return DEAMOE_ERR_WORKSPACE;
-  if (T == 0) return DEAMOE_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Events ev{events, n_events, 0, s};
   const deamoe_routing r = routing_in_ws(ws, L, routing_out);
@@ -404,12 +404,12 @@ int deamoe_route(const deamoe_config *cfg, int32_t T, const void *x, const void 
   const deamoe_config &c = *cfg;
   if (T < 0) return DEAMOE_ERR_INVALID;
   if (T > c.max_tokens) return DEAMOE_ERR_UNSUPPORTED;
+  if (T == 0) return DEAMOE_OK;   // empty batch: nothing to read or write
   if (!out || !routing_complete(*out)) return DEAMOE_ERR_INVALID;
   if (!logits_in && (!x || !router_w)) return DEAMOE_ERR_INVALID;
   if (router_w && ((uintptr_t)router_w & 15)) return DEAMOE_ERR_INVALID;
   const Layout L = make_layout(c);
   if (!ws || ws_bytes < L.total || (uintptr_t)ws % kAlign) return DEAMOE_ERR_WORKSPACE;
-  if (T == 0) return DEAMOE_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   Events ev{nullptr, 0, 0, s};
   const deamoe_routing r = routing_in_ws(ws, L, out);

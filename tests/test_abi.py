@@ -124,6 +124,7 @@ def test_layer_validation_paths():
     c = D.make_config(cfg, 16)
     Wt = weights_struct(cfg)
     assert call_layer(c, T=0, Wt=Wt) == D.OK                     # empty batch: no work
+    assert call_layer(c, T=0, Wt=None, x=None, y=None, ws=None) == D.OK
     assert call_layer(c, T=-1, Wt=Wt) == D.ERR_INVALID
     assert call_layer(c, T=17, Wt=Wt) == D.ERR_UNSUPPORTED       # beyond max_tokens
     assert call_layer(c, Wt=None) == D.ERR_INVALID
@@ -171,6 +172,7 @@ def test_route_validation():
     full = D.deamoe_routing(**{f: FAKE for f in D.ROUTING_FIELDS})
     n = D.workspace_bytes(c)
     assert L.deamoe_route(C.byref(c), 0, FAKE, FAKE, None, None, C.byref(full), FAKE, n, None) == D.OK
+    assert L.deamoe_route(C.byref(c), 0, None, None, None, None, None, None, 0, None) == D.OK
     assert L.deamoe_route(C.byref(c), 2, None, FAKE, None, None, C.byref(full), FAKE, n, None) == D.ERR_INVALID
     assert L.deamoe_route(C.byref(c), 2, FAKE, FAKE, None, None, None, FAKE, n, None) == D.ERR_INVALID
     assert L.deamoe_route(C.byref(c), 9, FAKE, FAKE, None, None, C.byref(full), FAKE, n, None) == D.ERR_UNSUPPORTED
