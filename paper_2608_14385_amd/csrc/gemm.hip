@@ -17,7 +17,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
   const int n_units = st.counts[0], n_tiles = st.counts[1];
   for (int u = threadIdx.x; u < n_units; u += blockDim.x) s_begin[u] = st.units[u].tile_begin;
   __syncthreads();
-  const int wave = threadIdx.x / kWave;
+  const int wave = uniform(threadIdx.x / kWave);
   for (int base = blockIdx.x * Run::TPB; base < n_tiles; base += gridDim.x * Run::TPB) {
     const int tile = base + wave / KS;
     const bool active = tile < n_tiles;
@@ -26,12 +26,13 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
       int lo = 0, hi = n_units - 1;
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (s_begin[mid] <= tile) lo = mid; else hi = mid - 1;
+        if (uniform(s_begin[mid]) <= tile) lo = mid; else hi = mid - 1;
       }
       u = lo;
     }
+    u = uniform(u);
     const GemmUnit *U = st.units + u;
-    Run::run(sm, U, active ? tile - s_begin[u] : 0, active, st.sigma);
+    Run::run(sm, U, active ? tile - uniform(s_begin[u]) : 0, active, st.sigma);
   }
 }
 
