@@ -21,7 +21,7 @@ int abytes_of(int act_dtype) { return act_dtype == DEAMOE_F32 ? 4 : 2; }
 
 // Number of hidden-dimension chunks the router product is split into: the
 // largest divisor of the K steps that keeps >= 4 steps per chunk (one per
-// wave) and about 256 workgroups in total.
+// wave), at most 16 chunks, and about 256 workgroups in total.
 int router_chunks(const deamoe_config &c) {
   const int ks = c.act_dtype == DEAMOE_F32 ? 64 : 128;
   const int steps = c.hidden / ks;
@@ -29,7 +29,7 @@ int router_chunks(const deamoe_config &c) {
   const int want = (256 + tiles - 1) / tiles;
   int best = 1;
   for (int d = 1; d <= steps; ++d)
-    if (steps % d == 0 && d <= want && steps / d >= 4) best = d;
+    if (steps % d == 0 && d <= want && d <= 16 && steps / d >= 4) best = d;
   return best;
 }
 
@@ -276,7 +276,7 @@ bool routing_complete(const deamoe_routing &r) {
 // Upper bound of the row tiles of a stage, for the grid size.
 int tiles_bound(int units_max, int R) { return units_max * ((R + kTile - 1) / kTile); }
 
-constexpr int kGridCap = 2048;   // 256 CUs x 8 workgroups
+constexpr int kGridCap = 8192;   // 256 CUs x 32 workgroups
 
 int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_weights *w,
                const float *logits_in, const float *bias, deamoe_routing *routing_out, void *y,
@@ -318,19 +318,19 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     const int ta = tiles_bound(act_depts, c.d_shared) +
                    (c.d_private ? tiles_bound(act_exps, c.d_private) : 0) +
                    se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, ntt, 4, ta, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, false, ntt, 4, ta, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
-    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 1, ntt, 1, tiles_bound(units, c.hidden), kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 1, false, ntt, 1, tiles_bound(units, c.hidden), kGridCap, s));
     DEAMOE_TRY(ev.mark());
   } else {
     const int d = c.d_shared;
     const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, ntt, 4, t0, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, false, ntt, 4, t0, kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, ntt, 4, tiles_bound(act_exps, d), kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, true, ntt, 4, tiles_bound(act_exps, d), kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(2), wt, 1, ntt, 4, tiles_bound(act_exps, d), kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(2), wt, 1, false, ntt, 4, tiles_bound(act_exps, d), kGridCap, s));
     DEAMOE_TRY(ev.mark());
     ZsumArgs za;
     za.counts = pc;
@@ -348,8 +348,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     za.act_f32 = c.act_dtype == DEAMOE_F32;
     DEAMOE_TRY(launch_zsum(za, T * dk, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(3), wt, 1, ntt, 1, tiles_bound(act_depts + se, c.hidden),
-                                   kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(3), wt, 1, false, ntt, 1,
+                                   tiles_bound(act_depts + se, c.hidden), kGridCap, s));
     DEAMOE_TRY(ev.mark());
   }
   CombineArgs ca;

@@ -9,9 +9,9 @@ namespace deamoe {
 
 constexpr int kMaxUnitsCached = 4096;
 
-template <int WT, int NW, int NTT, int KS>
+template <int WT, int NW, int NTT, int KS, bool SPLIT>
 __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
-  using Run = TileRunner<WT, NW, NTT, KS>;
+  using Run = TileRunner<WT, NW, NTT, KS, SPLIT>;
   __shared__ typename Run::Smem sm;
   __shared__ int32_t s_begin[kMaxUnitsCached];
   const int n_units = st.counts[0], n_tiles = st.counts[1];
@@ -37,47 +37,55 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
 }
 
 template <int WT, int NW, int NTT, int KS>
-static hipError_t launch_gemm(const GemmStage &st, int max_tiles, int grid_cap, hipStream_t s) {
+static hipError_t launch_gemm(const GemmStage &st, bool split, int max_tiles, int grid_cap,
+                              hipStream_t s) {
   constexpr int TPB = 4 / KS;
   int grid = (max_tiles + TPB - 1) / TPB;
   grid = grid < 1 ? 1 : (grid > grid_cap ? grid_cap : grid);
-  hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS>), dim3(grid), dim3(256), 0, s, st);
+  if constexpr (NW == 2) {
+    if (split) {
+      hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, true>), dim3(grid), dim3(256), 0, s, st);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false>), dim3(grid), dim3(256), 0, s, st);
   return hipGetLastError();
 }
 
 template <int WT, int NW, int KS>
-static hipError_t dispatch_ntt(const GemmStage &st, int ntt, int max_tiles, int cap, hipStream_t s) {
+static hipError_t dispatch_ntt(const GemmStage &st, bool split, int ntt, int max_tiles, int cap,
+                               hipStream_t s) {
   switch (ntt) {
-    case 1: return launch_gemm<WT, NW, 1, KS>(st, max_tiles, cap, s);
-    case 2: return launch_gemm<WT, NW, 2, KS>(st, max_tiles, cap, s);
-    case 4: return launch_gemm<WT, NW, 4, KS>(st, max_tiles, cap, s);
-    default: return launch_gemm<WT, NW, 8, KS>(st, max_tiles, cap, s);
+    case 1: return launch_gemm<WT, NW, 1, KS>(st, split, max_tiles, cap, s);
+    case 2: return launch_gemm<WT, NW, 2, KS>(st, split, max_tiles, cap, s);
+    case 4: return launch_gemm<WT, NW, 4, KS>(st, split, max_tiles, cap, s);
+    default: return launch_gemm<WT, NW, 8, KS>(st, split, max_tiles, cap, s);
   }
 }
 
 template <int WT, int NW>
-static hipError_t dispatch_ks(const GemmStage &st, int ntt, int ks, int max_tiles, int cap,
-                              hipStream_t s) {
+static hipError_t dispatch_ks(const GemmStage &st, bool split, int ntt, int ks, int max_tiles,
+                              int cap, hipStream_t s) {
   switch (ks) {
-    case 1: return dispatch_ntt<WT, NW, 1>(st, ntt, max_tiles, cap, s);
-    case 2: return dispatch_ntt<WT, NW, 2>(st, ntt, max_tiles, cap, s);
-    default: return dispatch_ntt<WT, NW, 4>(st, ntt, max_tiles, cap, s);
+    case 1: return dispatch_ntt<WT, NW, 1>(st, split, ntt, max_tiles, cap, s);
+    case 2: return dispatch_ntt<WT, NW, 2>(st, split, ntt, max_tiles, cap, s);
+    default: return dispatch_ntt<WT, NW, 4>(st, split, ntt, max_tiles, cap, s);
   }
 }
 
-hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int ntt, int ks,
-                               int max_tiles, int grid_cap, hipStream_t s) {
+hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, bool split, int ntt,
+                               int ks, int max_tiles, int grid_cap, hipStream_t s) {
   if (nw == 2) {
     switch (wtype) {
-      case WT_F32: return dispatch_ks<WT_F32, 2>(st, ntt, ks, max_tiles, grid_cap, s);
-      case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, ntt, ks, max_tiles, grid_cap, s);
-      default: return dispatch_ks<WT_FP8, 2>(st, ntt, ks, max_tiles, grid_cap, s);
+      case WT_F32: return dispatch_ks<WT_F32, 2>(st, split, ntt, ks, max_tiles, grid_cap, s);
+      case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, split, ntt, ks, max_tiles, grid_cap, s);
+      default: return dispatch_ks<WT_FP8, 2>(st, split, ntt, ks, max_tiles, grid_cap, s);
     }
   }
   switch (wtype) {
-    case WT_F32: return dispatch_ks<WT_F32, 1>(st, ntt, ks, max_tiles, grid_cap, s);
-    case WT_BF16: return dispatch_ks<WT_BF16, 1>(st, ntt, ks, max_tiles, grid_cap, s);
-    default: return dispatch_ks<WT_FP8, 1>(st, ntt, ks, max_tiles, grid_cap, s);
+    case WT_F32: return dispatch_ks<WT_F32, 1>(st, false, ntt, ks, max_tiles, grid_cap, s);
+    case WT_BF16: return dispatch_ks<WT_BF16, 1>(st, false, ntt, ks, max_tiles, grid_cap, s);
+    default: return dispatch_ks<WT_FP8, 1>(st, false, ntt, ks, max_tiles, grid_cap, s);
   }
 }
 

@@ -2,10 +2,16 @@
 //
 // One wave computes a 16-row tile of one or two weight matrices (gate and up
 // share the token operand) against up to 16 * NTT token rows, streaming the
-// weights from HBM exactly once.  Lane l owns weight row (l % 16) of the tile
-// and, in every K step, a contiguous run of K / 4 elements starting at
-// k0 + (l / 16) * (K_STEP / 4); the token operand is loaded with the same
-// K permutation, so the 16x16 matrix-core products sum over the whole step.
+// weights from HBM exactly once.
+//
+// Weight path per K step (WSEG bytes of each of the 16 rows): the rows are
+// read with whole-row-segment loads (each instruction covers RPI rows x WSEG
+// contiguous bytes, the pattern HBM streams fastest), staged through a
+// wave-private, padded LDS region and read back in the matrix-core operand
+// layout: lane (j = l % 16, g = l / 16) takes row j, and for product m the
+// bytes of k-range [32m + 8g, 32m + 8g + 8) (bf16, fp8) or the four fp32 of
+// [16m + 4g, 16m + 4g + 4).  The token operand uses the same K permutation,
+// so every 16x16 product sums over the whole step.
 //
 // Weight formats:
 //   WT_F32  fp32 weights, fp32 tokens:   v_mfma_f32_16x16x4_f32,  K_STEP 64
@@ -26,15 +32,26 @@ template <int WT>
 struct WTraits;
 template <>
 struct WTraits<WT_F32> {
-  static constexpr int K_STEP = 64, W_BYTES = 4, A_BYTES = 4, W_VEC = 4;
+  static constexpr int K_STEP = 64, W_BYTES = 4, A_BYTES = 4;
 };
 template <>
 struct WTraits<WT_BF16> {
-  static constexpr int K_STEP = 128, W_BYTES = 2, A_BYTES = 2, W_VEC = 4;
+  static constexpr int K_STEP = 128, W_BYTES = 2, A_BYTES = 2;
 };
 template <>
 struct WTraits<WT_FP8> {
-  static constexpr int K_STEP = 128, W_BYTES = 1, A_BYTES = 2, W_VEC = 2;
+  static constexpr int K_STEP = 128, W_BYTES = 1, A_BYTES = 2;
+};
+
+// Load geometry of one K step of a 16-row tile.
+template <int WT>
+struct WLoad {
+  static constexpr int WSEG = WTraits<WT>::K_STEP * WTraits<WT>::W_BYTES;   // bytes per row
+  static constexpr int LPR = WSEG / 16;      // lanes per row (16 B each)
+  static constexpr int RPI = 64 / LPR;       // rows per load instruction
+  static constexpr int NQ = kTile / RPI;     // load instructions per matrix
+  static constexpr int RS = WSEG + 16;       // padded LDS row stride
+  static constexpr int REGION = kTile * RS;  // LDS bytes per matrix per wave
 };
 
 __device__ inline bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -68,12 +85,8 @@ __device__ inline const char *token_row(const void *base, const int32_t *idx, in
 }
 
 // Byte offset, inside one K step of a token row, of the 16-byte token chunk
-// that pairs with matrix-core product q (q < 4) of lane group g.
-template <int WT>
-__device__ inline int b_chunk_offset(int g, int q) {
-  if constexpr (WT == WT_FP8) return (q >> 1) * 128 + g * 32 + (q & 1) * 16;
-  return q * 64 + g * 16;
-}
+// that pairs with matrix-core product m (m < 4) of lane group g.
+__device__ inline int b_chunk_offset(int g, int m) { return m * 64 + g * 16; }
 
 // Token operand of one K step for every token tile: B[tt][0..3] pairs with
 // gate / single weights, B[tt][4..7] with up weights when their inputs differ.
@@ -85,17 +98,17 @@ __device__ inline void load_b(u32x4 (&B)[NTT][SPLIT ? 8 : 4], const char *const 
     if (tt > 0 && tt >= ntt) break;   // ntt >= 1
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      B[tt][q] = *gptr(bp0[tt] + boff + b_chunk_offset<WT>(g, q));
-      if constexpr (SPLIT) B[tt][4 + q] = *gptr(bp1[tt] + boff + b_chunk_offset<WT>(g, q));
+      B[tt][q] = *gptr(bp0[tt] + boff + b_chunk_offset(g, q));
+      if constexpr (SPLIT) B[tt][4 + q] = *gptr(bp1[tt] + boff + b_chunk_offset(g, q));
     }
   }
 }
 
-// The matrix-core products of one K step.
+// The matrix-core products of one K step; a[n][m] is the operand of product
+// m (fp8: the first two dwords hold its eight codes).
 template <int WT, int NW, int NTT, bool SPLIT>
-__device__ inline void step_mma(const u32x4 (&a)[NW][WTraits<WT>::W_VEC],
-                                const u32x4 (&B)[NTT][SPLIT ? 8 : 4], int ntt, const float (&sc)[NW],
-                                f32x4 (&acc)[NW][NTT]) {
+__device__ inline void step_mma(const u32x4 (&a)[NW][4], const u32x4 (&B)[NTT][SPLIT ? 8 : 4],
+                                int ntt, const float (&sc)[NW], f32x4 (&acc)[NW][NTT]) {
 #pragma unroll
   for (int tt = 0; tt < NTT; ++tt) {
     if (tt > 0 && tt >= ntt) break;   // ntt >= 1
@@ -104,51 +117,57 @@ __device__ inline void step_mma(const u32x4 (&a)[NW][WTraits<WT>::W_VEC],
       const int bo = (SPLIT && n == 1) ? 4 : 0;
       if constexpr (WT == WT_BF16) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          acc[n][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a[n][q]),
-                                                               as_bf16x8(B[tt][bo + q]), acc[n][tt],
+        for (int m = 0; m < 4; ++m)
+          acc[n][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a[n][m]),
+                                                               as_bf16x8(B[tt][bo + m]), acc[n][tt],
                                                                0, 0, 0);
       } else if constexpr (WT == WT_FP8) {
         f32x4 t = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t lo = a[n][q >> 1][(q & 1) * 2], hi = a[n][q >> 1][(q & 1) * 2 + 1];
-          t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(lo, hi),
-                                                      as_bf16x8(B[tt][bo + q]), t, 0, 0, 0);
-        }
+        for (int m = 0; m < 4; ++m)
+          t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(a[n][m][0], a[n][m][1]),
+                                                      as_bf16x8(B[tt][bo + m]), t, 0, 0, 0);
         acc[n][tt] += sc[n] * t;
       } else {
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
+        for (int m = 0; m < 4; ++m)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            acc[n][tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[n][v][e]),
-                                                              __uint_as_float(B[tt][bo + v][e]),
+            acc[n][tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[n][m][e]),
+                                                              __uint_as_float(B[tt][bo + m][e]),
                                                               acc[n][tt], 0, 0, 0);
       }
     }
   }
 }
 
-// Accumulate the wave's tile over the K steps kp, kp + ks, ... of unit U.
-// Lane (j = l % 16, g = l / 16) owns weight row j of the tile; in each K step
-// its v-th 16-byte chunk sits at byte v * 64 + g * 16 of the row's step
-// segment, so every load instruction reads 64 contiguous bytes per row.
+// Stream one work item: row tiles rt0 .. rt0 + nsub - 1 of unit U, each over
+// the K steps kp, kp + ks, ... (nsub > 1 only when ks == 1).  `lds` is this
+// wave's private staging region (NW * WLoad<WT>::REGION bytes).
 // Rows past R and tokens past ntok are clamped to valid ones: their products
 // land only in output rows / columns that are never stored.
-// Software pipeline (loads retire in issue order): the token operand of a
-// step is requested before the weights two steps ahead, so waiting for it
-// never waits for the prefetched weights; two weight buffers alternate.
-template <int WT, int NW, int NTT, bool SPLIT>
-__device__ inline void tile_loop(const GemmUnit &U, int rt, int kp, int ks, f32x4 (&acc)[NW][NTT]) {
+// Software pipeline: loads retire in issue order, so the weights and the
+// token operand of one K step are requested together as one group, PF
+// groups ahead of the step being multiplied; waiting for a group never
+// waits for a later one.  Groups past the end read a cache-resident token
+// row instead of weights, so every iteration issues the same loads.
+// `done(rt, acc)` is called (and acc cleared) after the last K step of
+// each tile when nsub > 1; with nsub == 1 the caller finishes the tile.
+template <int WT, int NW, int NTT, bool SPLIT, int PF, class Done>
+__device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, int ks,
+                                 char *lds, f32x4 (&acc)[NW][NTT], Done done) {
   using Tr = WTraits<WT>;
+  using LD = WLoad<WT>;
+  constexpr int NB = PF + 1;
+  constexpr int BV = SPLIT ? 8 : 4;
+  constexpr int ASEG = Tr::K_STEP * Tr::A_BYTES;     // bytes of one token row per K step
   const int lane = lane_id();
   const int g = lane >> 4, j = lane & 15;
-  const int row = min(rt * kTile + j, U.R - 1);
-  const char *wp[NW];
-  wp[0] = static_cast<const char *>(U.w0) + (size_t)row * U.ldw * Tr::W_BYTES + g * 16;
-  if constexpr (NW == 2)
-    wp[1] = static_cast<const char *>(U.w1) + (size_t)row * U.ldw * Tr::W_BYTES + g * 16;
+  const int R = uniform(U.R), ldw = uniform(U.ldw);
+  const int nsteps = uniform(U.K / Tr::K_STEP);
+  const int nloc = kp < nsteps ? (nsteps - kp + ks - 1) / ks : 0;   // K steps of this wave per tile
+  const int total = nloc * nsub;
+  if (total == 0) return;
   const int ntt = uniform(min(NTT, (U.ntok + kTile - 1) / kTile));
   const char *bp0[NTT];
   const char *bp1[NTT];
@@ -159,66 +178,81 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt, int kp, int ks, f32x
     bp0[tt] = token_row(U.in0, U.idx, U.ldin, i, Tr::A_BYTES);
     bp1[tt] = SPLIT ? token_row(U.in1, U.idx, U.ldin, i, Tr::A_BYTES) : bp0[tt];
   }
-  const int nsteps = uniform(U.K / Tr::K_STEP);
-  constexpr int WSEG = Tr::K_STEP * Tr::W_BYTES;     // bytes of one row per K step
-  constexpr int ASEG = Tr::K_STEP * Tr::A_BYTES;     // bytes of one token row per K step
+  // load pattern: instruction q covers rows q * RPI + lane / LPR, 16 bytes each
+  const int lrow = lane / LD::LPR, lchunk = lane % LD::LPR;
+  const char *w0 = static_cast<const char *>(U.w0) + lchunk * 16;
+  const char *w1 = NW == 2 ? static_cast<const char *>(U.w1) + lchunk * 16 : w0;
+  const char *dummy = bp0[0] + (lane & 15) * 16;
   const int sblocks = U.K / 128;
-  const int srow = (rt * kTile) / 128;
-  if (kp >= nsteps) return;
-  u32x4 A0[NW][Tr::W_VEC], A1[NW][Tr::W_VEC];
-  u32x4 B[NTT][SPLIT ? 8 : 4];
-  // Past the last step the prefetch reads the first token row instead (a
-  // cache-resident address), so that every iteration issues the same loads.
-  const char *dummy = bp0[0] + g * 16;
-  auto load_w = [&](u32x4(&A)[NW][Tr::W_VEC], int step) {
-    const bool ok = step < nsteps;
+  u32x4 G[NB][NW][LD::NQ];
+  u32x4 B[NB][NTT][BV];
+  float SC[NB][NW];
+  // issue the load group of virtual step v (tile v / nloc, K step kp + (v % nloc) * ks)
+  auto issue = [&](u32x4(&Gb)[NW][LD::NQ], u32x4(&Bb)[NTT][BV], float (&sc)[NW], int v) {
+    const bool ok = v < total;
+    const int sub = ok ? v / nloc : 0;
+    const int kstep = ok ? kp + (v - sub * nloc) * ks : 0;
 #pragma unroll
-    for (int n = 0; n < NW; ++n) {
-      const char *p = ok ? wp[n] + (size_t)step * WSEG : dummy;
+    for (int q = 0; q < LD::NQ; ++q) {
+      const int row = min((rt0 + sub) * kTile + q * LD::RPI + lrow, R - 1);
+      const size_t woff = (size_t)row * ldw * Tr::W_BYTES + (size_t)kstep * LD::WSEG;
 #pragma unroll
-      for (int v = 0; v < Tr::W_VEC; ++v) A[n][v] = __builtin_nontemporal_load(gptr(p + v * 64));
+      for (int n = 0; n < NW; ++n)
+        Gb[n][q] = __builtin_nontemporal_load(gptr(ok ? (n ? w1 : w0) + woff : dummy));
     }
-  };
-  auto scales = [&](float (&sc)[NW], int step) {
+    load_b<WT, NTT, SPLIT>(Bb, bp0, bp1, ntt, (size_t)kstep * ASEG, g);
     if constexpr (WT == WT_FP8) {
-      sc[0] = U.s0[srow * sblocks + step];
-      if constexpr (NW == 2) sc[1] = U.s1[srow * sblocks + step];
+      const int srow = ((rt0 + sub) * kTile) / 128;
+      sc[0] = U.s0[srow * sblocks + kstep];
+      if constexpr (NW == 2) sc[1] = U.s1[srow * sblocks + kstep];
     }
   };
-  float sc[NW];
-  // sched_barrier keeps the backend from sinking the prefetch next to its use.
-  load_w(A0, kp);
-  load_b<WT, NTT, SPLIT>(B, bp0, bp1, ntt, (size_t)kp * ASEG, g);
-  scales(sc, kp);
-  load_w(A1, kp + ks);
-  __builtin_amdgcn_sched_barrier(0);
-  for (int s = kp;;) {
-    step_mma<WT, NW, NTT, SPLIT>(A0, B, ntt, sc, acc);
-    s += ks;
-    if (s >= nsteps) break;
+  // rows of the staged step in the matrix-core operand layout
+  auto stage = [&](const u32x4(&Gb)[NW][LD::NQ], u32x4(&a)[NW][4]) {
+#pragma unroll
+    for (int n = 0; n < NW; ++n)
+#pragma unroll
+      for (int q = 0; q < LD::NQ; ++q)
+        *reinterpret_cast<u32x4 *>(lds + n * LD::REGION + (q * LD::RPI + lrow) * LD::RS +
+                                       lchunk * 16) = Gb[n][q];
     __builtin_amdgcn_sched_barrier(0);
-    load_b<WT, NTT, SPLIT>(B, bp0, bp1, ntt, (size_t)s * ASEG, g);
-    scales(sc, s);
-    load_w(A0, s + ks);
-    __builtin_amdgcn_sched_barrier(0);
-    step_mma<WT, NW, NTT, SPLIT>(A1, B, ntt, sc, acc);
-    s += ks;
-    if (s >= nsteps) break;
-    __builtin_amdgcn_sched_barrier(0);
-    load_b<WT, NTT, SPLIT>(B, bp0, bp1, ntt, (size_t)s * ASEG, g);
-    scales(sc, s);
-    load_w(A1, s + ks);
-    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int n = 0; n < NW; ++n)
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        if constexpr (WT == WT_FP8) {
+          const u32x2 v = *reinterpret_cast<const u32x2 *>(lds + n * LD::REGION + j * LD::RS +
+                                                             m * 32 + g * 8);
+          a[n][m] = u32x4{v[0], v[1], 0u, 0u};
+        } else {
+          a[n][m] = *reinterpret_cast<const u32x4 *>(lds + n * LD::REGION + j * LD::RS +
+                                                        b_chunk_offset(g, m));
+        }
+      }
+  };
+#pragma unroll
+  for (int p = 0; p < PF; ++p) issue(G[p], B[p], SC[p], p);
+  for (int v = 0;;) {
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      const int qn = (q + NB - 1) % NB;   // the buffer consumed one step ago
+      issue(G[qn], B[qn], SC[qn], v + PF);
+      __builtin_amdgcn_sched_barrier(0);
+      u32x4 a[NW][4];
+      stage(G[q], a);
+      step_mma<WT, NW, NTT, SPLIT>(a, B[q], ntt, SC[q], acc);
+      __builtin_amdgcn_sched_barrier(0);
+      ++v;
+      if (nsub > 1 && v % nloc == 0) {   // a tile of a multi-tile work item is complete
+        done(rt0 + v / nloc - 1, acc);
+#pragma unroll
+        for (int n = 0; n < NW; ++n)
+#pragma unroll
+          for (int tt = 0; tt < NTT; ++tt) acc[n][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      if (v >= total) return;
+    }
   }
-}
-
-template <int WT, int NW, int NTT>
-__device__ inline void tile_compute(const GemmUnit &U, int rt, int kp, int ks,
-                                    f32x4 (&acc)[NW][NTT]) {
-  if (NW == 2 && U.in1 != U.in0)
-    tile_loop<WT, NW, NTT, true>(U, rt, kp, ks, acc);
-  else
-    tile_loop<WT, NW, NTT, false>(U, rt, kp, ks, acc);
 }
 
 // Four consecutive outputs (fp32 or bf16) at element offset off; `full`
@@ -288,43 +322,68 @@ __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int sigma, const
   }
 }
 
-// One workgroup of 4 waves: 4 / KS tiles, each split over KS waves along K
-// (interleaved K steps), partial tiles summed in a fixed order through LDS.
-template <int WT, int NW, int NTT, int KS>
+// One workgroup of 4 waves: 4 / KS work items, each split over KS waves
+// along K (interleaved K steps, partial tiles summed in a fixed order
+// through LDS; work items of one tile), or with KS == 1 one work item of
+// `tpg` tiles per wave.
+// SPLIT: the two matrices read different token operands (in0 / in1).
+#ifndef DEAMOE_PF_NW1
+#define DEAMOE_PF_NW1 1
+#endif
+#ifndef DEAMOE_PF_NW2
+#define DEAMOE_PF_NW2 1
+#endif
+template <int WT, int NW, int NTT, int KS, bool SPLIT = false>
 struct TileRunner {
   static constexpr int TPB = 4 / KS;
+  // load groups in flight per wave
+  static constexpr int PF = NTT > 2 ? 1 : (NW == 1 ? DEAMOE_PF_NW1 : DEAMOE_PF_NW2);
+  static constexpr int STAGE_BYTES = NW * WLoad<WT>::REGION;   // per wave
+  static constexpr int RED_BYTES = KS > 1 ? NW * NTT * kWave * 16 : 0;   // per wave
+  static constexpr int WAVE_BYTES = STAGE_BYTES > RED_BYTES ? STAGE_BYTES : RED_BYTES;
   struct Smem {
-    f32x4 red[KS > 1 ? 4 : 1][NW * NTT][kWave];
+    alignas(16) char buf[4][WAVE_BYTES];   // staging, then (KS > 1) partial tiles
   };
 
-  __device__ static void run(Smem &sm, const GemmUnit *U, int rt, bool active, int sigma) {
+  __device__ static void run(Smem &sm, const GemmUnit *U, int item, bool active, int sigma) {
     const int wave = uniform(threadIdx.x / kWave), lane = lane_id();
     const int kp = uniform(wave % KS);
-    rt = uniform(rt);
+    item = uniform(item);
     f32x4 acc[NW][NTT];
 #pragma unroll
     for (int n = 0; n < NW; ++n)
 #pragma unroll
       for (int tt = 0; tt < NTT; ++tt) acc[n][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (active) tile_compute<WT, NW, NTT>(*U, rt, kp, KS, acc);
+    int rt0 = 0, nsub = 1;
+    if (active) {
+      const int tpg = KS == 1 ? uniform(U->tpg) : 1;
+      const int ntiles = (uniform(U->R) + kTile - 1) / kTile;
+      rt0 = item * tpg;
+      nsub = min(tpg, ntiles - rt0);
+      auto done = [&](int rt, const f32x4 (&a)[NW][NTT]) { tile_epilogue<NW, NTT>(*U, rt, sigma, a); };
+      tile_loop<WT, NW, NTT, SPLIT, PF>(*U, rt0, nsub, kp, KS, sm.buf[wave], acc, done);
+    }
     if constexpr (KS > 1) {
+      f32x4 *red = reinterpret_cast<f32x4 *>(sm.buf[wave]);
       if (active && kp > 0) {
 #pragma unroll
         for (int n = 0; n < NW; ++n)
 #pragma unroll
-          for (int tt = 0; tt < NTT; ++tt) sm.red[wave][n * NTT + tt][lane] = acc[n][tt];
+          for (int tt = 0; tt < NTT; ++tt) red[(n * NTT + tt) * kWave + lane] = acc[n][tt];
       }
       __syncthreads();
       if (active && kp == 0) {
-        for (int q = 1; q < KS; ++q)
+        for (int q = 1; q < KS; ++q) {
+          const f32x4 *r = reinterpret_cast<const f32x4 *>(sm.buf[wave + q]);
 #pragma unroll
           for (int n = 0; n < NW; ++n)
 #pragma unroll
-            for (int tt = 0; tt < NTT; ++tt) acc[n][tt] += sm.red[wave + q][n * NTT + tt][lane];
+            for (int tt = 0; tt < NTT; ++tt) acc[n][tt] += r[(n * NTT + tt) * kWave + lane];
+        }
       }
       __syncthreads();
     }
-    if (active && kp == 0) tile_epilogue<NW, NTT>(*U, rt, sigma, acc);
+    if (active && kp == 0 && nsub == 1) tile_epilogue<NW, NTT>(*U, rt0, sigma, acc);
   }
 };
 

@@ -25,6 +25,7 @@ enum Epilogue : int32_t {
 };
 
 // One weight matrix (or gate/up pair) applied to a group of token rows.
+// A work item is `tpg` consecutive 16-row tiles of the unit.
 // Row r of the weights is at w + r * ldw (elements of the weight type).  The
 // B operand row of token i is at in + idx[i] * ldin (idx == NULL: row i).
 // Output row of token i is at out + i * ldout (act type or fp32).
@@ -35,10 +36,10 @@ struct GemmUnit {
   const int32_t *idx;
   void *out0, *out1;
   int32_t R, K, ldw, ldin, ldout, ntok;
-  int32_t tile_begin;       // exclusive prefix of row tiles over the units of a stage
+  int32_t tile_begin;       // exclusive prefix of work items over the units of a stage
   int32_t epi;              // Epilogue
   int32_t out_f32;          // 1: outputs are fp32, 0: act dtype
-  int32_t pad_;
+  int32_t tpg;              // row tiles per work item (1 unless the K split is 1)
 };
 
 struct GemmStage {

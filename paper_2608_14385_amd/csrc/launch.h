@@ -68,8 +68,9 @@ struct ZsumArgs {
 
 hipError_t launch_router(const RouterArgs &a, int wtype, int ntt, int kc, hipStream_t s);
 hipError_t launch_route_plan(const RouteArgs &a, hipStream_t s);
-hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int ntt, int ks,
-                               int max_tiles, int grid_cap, hipStream_t s);
+// split: the stage's two matrices read different token operands (in0 / in1).
+hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, bool split, int ntt,
+                               int ks, int max_tiles, int grid_cap, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 hipError_t launch_zsum(const ZsumArgs &a, int max_dept_pairs, hipStream_t s);
 

@@ -40,6 +40,7 @@ __global__ __launch_bounds__(256) void router_kernel(RouterArgs a) {
   U.ntok = a.T;
   U.epi = EPI_STORE;
   U.out_f32 = 1;
+  U.tpg = 1;
   Run::run(sm, &U, rt, true, DEAMOE_SIGMA_NONE);
 }
 
@@ -65,14 +66,48 @@ __device__ inline bool ranks_before(float va, int a, float vb, int b) {
   return va > vb || (va == vb && a < b);
 }
 
-// Wave-wide arg-max by (value desc, index asc); every lane gets the winner.
-__device__ inline void wave_argmax(float &v, int &i) {
+// Order-preserving map of a float onto an unsigned int (larger float, larger key).
+__device__ inline uint32_t ord_u32(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Wave-wide maximum of a 64-bit key, returned to every lane: DPP exchanges
+// within each row of 16 lanes (xor 1, xor 2, half-row mirror, row mirror),
+// then the four row maxima through readlane.
+__device__ inline uint64_t wave_max_u64(uint64_t v) {
+#define DEAMOE_DPP_STEP(ctrl)                                                               \
+  do {                                                                                      \
+    const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);                              \
+    const uint32_t olo = __builtin_amdgcn_update_dpp(lo, lo, ctrl, 0xf, 0xf, false);        \
+    const uint32_t ohi = __builtin_amdgcn_update_dpp(hi, hi, ctrl, 0xf, 0xf, false);        \
+    const uint64_t o = ((uint64_t)ohi << 32) | olo;                                         \
+    v = o > v ? o : v;                                                                      \
+  } while (0)
+  DEAMOE_DPP_STEP(0xB1);    // quad_perm [1,0,3,2]
+  DEAMOE_DPP_STEP(0x4E);    // quad_perm [2,3,0,1]
+  DEAMOE_DPP_STEP(0x141);   // row_half_mirror
+  DEAMOE_DPP_STEP(0x140);   // row_mirror
+#undef DEAMOE_DPP_STEP
+  uint64_t best = 0;
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float ov = __shfl_xor(v, off);
-    const int oi = __shfl_xor(i, off);
-    if (ranks_before(ov, oi, v, i)) { v = ov; i = oi; }
+  for (int r = 0; r < 4; ++r) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, 16 * r);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), 16 * r);
+    const uint64_t o = ((uint64_t)hi << 32) | lo;
+    best = o > best ? o : best;
   }
+  return best;
+}
+
+// Arg-max by (value desc, index asc) over the lanes' candidates; a lane with
+// no candidate passes valid = false.  Returns the winning index (every lane).
+__device__ inline int wave_argmax_idx(float v, int i, bool valid, float &best_v) {
+  const uint64_t key = valid ? (((uint64_t)ord_u32(v) << 32) | (uint32_t)~(uint32_t)i) : 0ull;
+  const uint64_t b = wave_max_u64(key);
+  const uint32_t ob = (uint32_t)(b >> 32);
+  best_v = __uint_as_float((ob & 0x80000000u) ? (ob & 0x7fffffffu) : ~ob);
+  return (int)~(uint32_t)b;
 }
 
 __device__ inline float wave_sum(float v) {
@@ -138,46 +173,93 @@ __device__ inline void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-constexpr int kSlots = kMaxN / 64;   // logits per lane (n <= 2048)
+constexpr int kMaxKC = 16;   // router chunks (host caps the split)
 
-__global__ __launch_bounds__(kRouteThreads) void route_plan_kernel(RouteArgs a) {
-  __shared__ int32_t s_ids[kMaxTK];
-  __shared__ float s_w[kMaxTK];
-  __shared__ int32_t s_dep[kMaxTK];
-  __shared__ float s_dw[kMaxTK];
-  __shared__ int32_t s_pair[kMaxTK];          // dept pair index of (t, dept slot)
-  __shared__ uint32_t s_ebits[kMaxT * (kMaxN / 32)];
+// Fill one unit of a stage table field by field (no temporary struct).
+__device__ inline void put_unit(GemmUnit *U, const void *w0, const void *w1, const float *s0,
+                                const float *s1, const void *in0, const void *in1,
+                                const int32_t *idx, void *out0, void *out1, int R, int K, int ldin,
+                                int ldout, int ntok, int tile_begin, int epi, int out_f32,
+                                int tpg = 1) {
+  U->w0 = w0; U->w1 = w1; U->s0 = s0; U->s1 = s1; U->in0 = in0; U->in1 = in1; U->idx = idx;
+  U->out0 = out0; U->out1 = out1; U->R = R; U->K = K; U->ldw = K; U->ldin = ldin;
+  U->ldout = ldout; U->ntok = ntok; U->tile_begin = tile_begin; U->epi = epi;
+  U->out_f32 = out_f32; U->tpg = tpg;
+}
+
+// Row tiles per work item of a stage whose K is not split across waves: short
+// contractions take several tiles so that a work item streams enough bytes.
+__device__ inline int tiles_per_item(int K) { return max(1, min(8, 2048 / K)); }
+__device__ inline int items_of(int R, int tpg) { return ((R + kTile - 1) / kTile + tpg - 1) / tpg; }
+
+__device__ inline bool bit_at(const uint32_t *row, int i) { return (row[i >> 5] >> (i & 31)) & 1; }
+
+// Number of set bits below bit i of a bitmap row.
+__device__ inline int rank_below(const uint32_t *row, int i) {
+  int r = 0;
+  for (int w = 0; w < (i >> 5); ++w) r += __popc(row[w]);
+  return r + __popc(row[i >> 5] & ((1u << (i & 31)) - 1u));
+}
+
+constexpr int kTW = kMaxT / 32;   // words of a token bitmap
+constexpr int kDW = kMaxM / 32;   // words of a department bitmap
+
+// NS: logits held per lane (n <= 64 * NS); BT: threads of the workgroup.
+//
+// Membership is kept as bitmaps in LDS: for every expert and department the
+// set of its tokens (kTW words), for every token the set of its departments.
+// A token's position in a CSR list is then the offset of the list plus the
+// number of member tokens below it, so every (token, rank) pair is placed
+// independently and the lists come out in ascending token order.
+template <int NS, int BT>
+__global__ __launch_bounds__(BT) void route_plan_kernel(RouteArgs a) {
+  constexpr int EPT = kMaxN / BT;   // experts per thread in the per-expert loops
+  __shared__ int32_t s_ids[kMaxTK];            // [t][rank] selected expert
+  __shared__ int32_t s_dep[kMaxTK];            // [t][slot] departments, ascending
+  __shared__ uint32_t s_etok[kMaxN * kTW];     // [e] token bitmap
+  __shared__ uint32_t s_dtok[kMaxM * kTW];     // [j] token bitmap
+  __shared__ uint32_t s_dbits[kMaxT * kDW];    // [t] department bitmap
   __shared__ int32_t s_dcnt[kMaxM + 1];
   __shared__ int32_t s_ecnt[kMaxN + 1];
   __shared__ int32_t s_nd[kMaxT];
-  __shared__ int32_t s_gs[kRouteThreads / 64][kMaxMGrouped];
+  __shared__ int32_t s_gs[BT / 64][kMaxMGrouped];
   __shared__ int32_t s_tmp[64];
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int T = a.T, n = a.n, m = a.m, k = a.k, E = a.E;
-  const int nwords = (n + 31) / 32;
-  for (int i = tid; i < T * nwords; i += blockDim.x) s_ebits[i] = 0;
+  const int tw = (T + 31) / 32, dwords = (m + 31) / 32;
+  const bool slice = a.plan == PLAN_SLICE;
+  const bool exp_slots = slice && a.d_p > 0;
+  const int S = a.max_slots;
+  for (int i = tid; i < n * kTW; i += BT) s_etok[i] = 0;
+  for (int i = tid; i < m * kTW; i += BT) s_dtok[i] = 0;
+  for (int i = tid; i < T * dwords; i += BT) s_dbits[i] = 0;
   __syncthreads();
 
-  // ---------------------------------------------------------------- phase 1
-  for (int t = wave; t < T; t += kRouteThreads / 64) {
-    float lv[kSlots];
+  // ------------------------------------------------ phase 1: one wave per token
+  for (int t = wave; t < T; t += BT / 64) {
+    float lv[NS];
 #pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
+    for (int s = 0; s < NS; ++s) {
       const int e = lane + 64 * s;
-      lv[s] = -INFINITY;
-      if (e < n) {
-        float l;
-        if (a.logits_in) {
-          l = a.logits_in[(size_t)t * n + e];
-        } else {
-          l = a.part[(size_t)t * n + e];
-          for (int c = 1; c < a.kc; ++c) l += a.part[((size_t)c * T + t) * n + e];
-        }
-        if (a.bias) l = l + a.bias[e];
-        a.r.logits[(size_t)t * n + e] = l;
-        lv[s] = (l != l) ? -INFINITY : l;   // NaN ranks last
+      const int ec = e < n ? e : n - 1;
+      float l;
+      if (a.logits_in) {
+        l = a.logits_in[(size_t)t * n + ec];
+      } else {  // partial sums of the router chunks, added in chunk order; all
+                // loads are issued first (chunks past kc re-read the last one)
+        float pc[kMaxKC];
+#pragma unroll
+        for (int c = 0; c < kMaxKC; ++c)
+          pc[c] = a.part[((size_t)min(c, a.kc - 1) * T + t) * n + ec];
+        l = pc[0];
+#pragma unroll
+        for (int c = 1; c < kMaxKC; ++c) l = c < a.kc ? l + pc[c] : l;
       }
+      if (a.bias) l = l + a.bias[ec];
+      if (e < n) a.r.logits[(size_t)t * n + e] = l;
+      lv[s] = (e < n && l == l) ? l : -INFINITY;   // NaN ranks last
     }
     // group-limited top-k: keep the kdept departments with the largest
     // maximum logit (ties to the lower department id)
@@ -186,7 +268,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_plan_kernel(RouteArgs a) 
       if (lane < m) s_gs[wave][lane] = ord_key(-INFINITY);
       wave_lds_sync();
 #pragma unroll
-      for (int s = 0; s < kSlots; ++s) {
+      for (int s = 0; s < NS; ++s) {
         const int e = lane + 64 * s;
         if (e < n) atomicMax(&s_gs[wave][e / E], ord_key(lv[s]));
       }
@@ -194,11 +276,9 @@ __global__ __launch_bounds__(kRouteThreads) void route_plan_kernel(RouteArgs a) 
       const float gsv = lane < m ? ord_val(s_gs[wave][lane]) : -INFINITY;
       keep = 0;
       for (int r = 0; r < a.kdept; ++r) {
-        float bv = -INFINITY;
-        int bj = 0x7fffffff;
-        if (lane < m && !((keep >> lane) & 1)) { bv = gsv; bj = lane; }
-        wave_argmax(bv, bj);
-        keep |= 1ull << bj;
+        float bv;
+        const int bj = wave_argmax_idx(gsv, lane, lane < m && !((keep >> lane) & 1), bv);
+        keep |= 1ull << (bj & 63);
       }
     }
     // top-k: k rounds of arg-max over the lane-held logits
@@ -209,13 +289,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_plan_kernel(RouteArgs a) 
       float bv = -INFINITY;
       int be = 0x7fffffff;
 #pragma unroll
-      for (int s = 0; s < kSlots; ++s) {
+      for (int s = 0; s < NS; ++s) {
         const int e = lane + 64 * s;
-        const bool ok = e < n && !((taken >> s) & 1) && ((keep >> ((e / E) & 63)) & 1 || a.kdept == 0);
+        const bool ok = e < n && !((taken >> s) & 1) &&
+                        (a.kdept == 0 || ((keep >> ((e / E) & 63)) & 1));
         if (ok && ranks_before(lv[s], e, bv, be)) { bv = lv[s]; be = e; }
       }
-      wave_argmax(bv, be);
-      if (be >= n) be = 0;   // unreachable: at least k experts are always eligible
+      be = wave_argmax_idx(bv, be, be != 0x7fffffff, bv);
+      if (be < 0 || be >= n) be = 0;   // unreachable: at least k experts are always eligible
       if ((be & 63) == lane) taken |= 1u << (be >> 6);
       if (lane == r) { my_id = be; my_l = bv; }
     }
@@ -230,78 +311,81 @@ __global__ __launch_bounds__(kRouteThreads) void route_plan_kernel(RouteArgs a) 
       } else {
         float lm = -INFINITY;
 #pragma unroll
-        for (int s = 0; s < kSlots; ++s) lm = fmaxf(lm, lv[s]);
+        for (int s = 0; s < NS; ++s) lm = fmaxf(lm, lv[s]);
         mx = wave_max(lm);
         float ls = 0.f;
 #pragma unroll
-        for (int s = 0; s < kSlots; ++s)
+        for (int s = 0; s < NS; ++s)
           if (lane + 64 * s < n) ls += expf(lv[s] - mx);
         den = wave_sum(ls);
       }
       p = expf(my_l - mx) / den;
     } else {
       const float sg = 1.0f / (1.0f + expf(-my_l));
-      if (a.renorm) {
-        const float den = wave_sum(sel ? sg : 0.f);
-        p = sg / den;
-      } else {
-        p = sg;
-      }
+      p = a.renorm ? sg / wave_sum(sel ? sg : 0.f) : sg;
     }
     p *= a.route_scale;
+    const int d = sel ? my_id / E : 0;
     if (sel) {
       a.r.topk_ids[t * k + lane] = my_id;
       a.r.topk_w[t * k + lane] = p;
       s_ids[t * k + lane] = my_id;
-      s_w[t * k + lane] = p;
-      atomicOr(&s_ebits[t * nwords + (my_id >> 5)], 1u << (my_id & 31));
+      atomicOr(&s_etok[my_id * kTW + (t >> 5)], 1u << (t & 31));
+      atomicOr(&s_dtok[d * kTW + (t >> 5)], 1u << (t & 31));
+      atomicOr(&s_dbits[t * dwords + (d >> 5)], 1u << (d & 31));
     }
-    // distinct departments, ascending, with the summed weight in rank order
-    const int d = sel ? my_id / E : 0x7fffffff;
-    uint32_t eq = 0;
-    for (int q = 0; q < k; ++q) eq |= (uint32_t)(__shfl(d, q) == d) << q;
-    const bool first = sel && (eq & ((1u << lane) - 1u)) == 0;   // no earlier rank in d
-    int pos = 0;
+    wave_lds_sync();
+    // distinct departments, ascending, each with the weights of its selected
+    // experts summed in rank order
+    const uint32_t *drow = s_dbits + t * dwords;
+    int nd = 0;
+    for (int w = 0; w < dwords; ++w) nd += __popc(drow[w]);
+    nd = __builtin_amdgcn_readfirstlane(nd);
     float P = 0.f;
+    uint32_t eq = 0;
     for (int q = 0; q < k; ++q) {
-      const int dq = __shfl(d, q);
-      const bool fq = __shfl((int)first, q) != 0;
-      const float pq = __shfl(p, q);
-      pos += (fq && dq < d) ? 1 : 0;
-      if (dq == d) P += pq;
+      const int dq = __builtin_amdgcn_readlane(d, q);
+      const float pq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), q));
+      if (dq == d) { P += pq; eq |= 1u << q; }
     }
-    const int nd = __popcll(__ballot(first));
+    const bool first = sel && (eq & ((1u << lane) - 1u)) == 0;
     if (first) {
+      const int pos = rank_below(drow, d);
       a.r.tok_depts[t * k + pos] = d;
       a.r.tok_dept_w[t * k + pos] = P;
       s_dep[t * k + pos] = d;
-      s_dw[t * k + pos] = P;
+      if (a.plan) a.slot_w[(size_t)t * S + pos] = slice ? P : 1.0f;
     }
     if (lane >= nd && lane < k) {
       a.r.tok_depts[t * k + lane] = -1;
       a.r.tok_dept_w[t * k + lane] = 0.f;
     }
+    if (a.plan && exp_slots && sel) a.slot_w[(size_t)t * S + nd + lane] = p;
     if (lane == 0) {
       a.r.tok_ndept[t] = nd;
       s_nd[t] = nd;
+      if (a.plan) {
+        const int ns = nd + (exp_slots ? k : 0);
+        if (a.d_se > 0) a.slot_w[(size_t)t * S + ns] = 1.0f;
+        a.nslot[t] = ns + (a.d_se > 0 ? 1 : 0);
+      }
     }
   }
   __syncthreads();
 
-  // ---------------------------------------------------------------- phase 2
-  // counts: department j is touched by token t when j is among its departments
-  int my_dc = 0, my_ec[2] = {0, 0};
+  // ------------------------------------------------ phase 2: counts and lists
+  int my_dc = 0, my_ec[EPT] = {};
   if (tid < m) {
-    for (int t = 0; t < T; ++t)
-      for (int r = 0; r < s_nd[t]; ++r) my_dc += s_dep[t * k + r] == tid;
+    for (int w = 0; w < tw; ++w) my_dc += __popc(s_dtok[tid * kTW + w]);
     s_dcnt[tid] = my_dc;
     a.r.dept_count[tid] = my_dc;
   }
-  for (int q = 0; q < 2; ++q) {
-    const int e = tid + q * kRouteThreads;
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    const int e = tid + q * BT;
     if (e < n) {
       int c = 0;
-      for (int t = 0; t < T; ++t) c += (s_ebits[t * nwords + (e >> 5)] >> (e & 31)) & 1;
+      for (int w = 0; w < tw; ++w) c += __popc(s_etok[e * kTW + w]);
       my_ec[q] = c;
       s_ecnt[e] = c;
       a.r.exp_count[e] = c;
@@ -310,169 +394,163 @@ __global__ __launch_bounds__(kRouteThreads) void route_plan_kernel(RouteArgs a) 
   __syncthreads();
   const int ndp = block_exscan(s_dcnt, m, s_tmp);
   const int nep = block_exscan(s_ecnt, n, s_tmp);
+  const bool has_priv = a.plan == PLAN_FACTORED || a.d_p > 0;
+  const bool has_se = a.d_se > 0;
+  const int nep_priv = has_priv ? nep : 0;
   if (tid < m) a.r.dept_offset[tid] = s_dcnt[tid];
-  for (int e = tid; e < n; e += kRouteThreads) a.r.exp_offset[e] = s_ecnt[e];
+  for (int e = tid; e < n; e += BT) a.r.exp_offset[e] = s_ecnt[e];
   if (tid == 0) {
     a.r.dept_offset[m] = ndp;
     a.r.exp_offset[n] = nep;
   }
-  // department token lists (ascending t); remember each (t, dept slot)'s pair
-  const int my_doff = tid < m ? s_dcnt[tid] : 0;
-  if (tid < m) {
-    int pos = my_doff;
-    for (int t = 0; t < T; ++t)
-      for (int r = 0; r < s_nd[t]; ++r)
-        if (s_dep[t * k + r] == tid) {
-          a.r.dept_tokens[pos] = t;
-          s_pair[t * k + r] = pos;
-          ++pos;
-        }
-  }
-  __syncthreads();
-  int my_eoff[2] = {0, 0};
-  for (int q = 0; q < 2; ++q) {
-    const int e = tid + q * kRouteThreads;
-    if (e >= n) continue;
-    my_eoff[q] = s_ecnt[e];
-    int pos = my_eoff[q];
-    for (int t = 0; t < T; ++t) {
-      if (!((s_ebits[t * nwords + (e >> 5)] >> (e & 31)) & 1)) continue;
-      a.r.exp_tokens[pos] = t;
-      int r = 0;
-      while (r < k - 1 && s_ids[t * k + r] != e) ++r;
-      if (a.plan) {
-        a.tok_exp_pair[t * k + r] = pos;
-        if (a.plan == PLAN_FACTORED) {
-          int q2 = 0;
-          while (q2 < s_nd[t] - 1 && s_dep[t * k + q2] != e / E) ++q2;
-          a.exp_src[pos] = s_pair[t * k + q2];
-        }
+  // every (token, rank) pair places itself: the expert of that rank and, for
+  // ranks below the token's department count, the department of that slot
+  for (int idx = tid; idx < T * k; idx += BT) {
+    const int t = idx / k, q = idx - t * k;
+    const int e = s_ids[idx];
+    const int pe = s_ecnt[e] + rank_below(s_etok + e * kTW, t);
+    a.r.exp_tokens[pe] = t;
+    if (a.plan) {
+      a.tok_exp_pair[idx] = pe;
+      if (exp_slots) a.slot_pair[(size_t)t * S + s_nd[t] + q] = ndp + pe;
+      if (a.plan == PLAN_FACTORED) {
+        const int j = e / E;
+        a.exp_src[pe] = s_dcnt[j] + rank_below(s_dtok + j * kTW, t);
       }
-      ++pos;
+    }
+    if (q < s_nd[t]) {
+      const int j = s_dep[idx];
+      const int pd = s_dcnt[j] + rank_below(s_dtok + j * kTW, t);
+      a.r.dept_tokens[pd] = t;
+      if (a.plan) a.slot_pair[(size_t)t * S + q] = pd;
     }
   }
+  if (a.plan && has_se)
+    for (int t = tid; t < T; t += BT)
+      a.slot_pair[(size_t)t * S + s_nd[t] + (exp_slots ? k : 0)] = ndp + (slice ? nep_priv : 0) + t;
   if (!a.plan) return;
+  const int my_doff = tid < m ? s_dcnt[tid] : 0;
+  int my_eoff[EPT] = {};
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    const int e = tid + q * BT;
+    if (e < n) my_eoff[q] = s_ecnt[e];
+  }
   __syncthreads();
 
-  // ---------------------------------------------------------------- phase 3
-  const bool has_priv = a.plan == PLAN_FACTORED || a.d_p > 0;
-  const bool has_se = a.d_se > 0;
+  // ------------------------------------------------ phase 3: stage unit tables
   // unit index of every active department / expert (prefix over active flags)
   if (tid < m) s_dcnt[tid] = my_dc > 0;
-  for (int q = 0; q < 2; ++q) {
-    const int e = tid + q * kRouteThreads;
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    const int e = tid + q * BT;
     if (e < n) s_ecnt[e] = has_priv && my_ec[q] > 0;
   }
   __syncthreads();
   const int ud = block_exscan(s_dcnt, m, s_tmp);
   const int ue = block_exscan(s_ecnt, n, s_tmp);
-  const int th = (a.h + kTile - 1) / kTile;
-  const int nep_priv = has_priv ? nep : 0;
   const int wb = a.w_bytes, ab = a.act_f32 ? 4 : 2;
   const char *x = static_cast<const char *>(a.x);
-  auto wptr = [&](const void *base, int idx, int R, int C) {
+  auto wptr = [&](const void *base, int idx, int R, int C) -> const void * {
     return static_cast<const char *>(base) + (size_t)idx * R * C * wb;
   };
   auto sptr = [&](const float *base, int idx, int R, int C) -> const float * {
     if (!a.fp8) return nullptr;
     return base + (size_t)idx * ((R + 127) / 128) * (C / 128);
   };
-  auto make = [&](const void *w0, const void *w1, const float *s0, const float *s1, const void *in0,
-                  const void *in1, const int32_t *idx, void *out0, void *out1, int R, int K,
-                  int ldin, int ldout, int ntok, int tile_begin, int epi, int out_f32) {
-    GemmUnit U;
-    U.w0 = w0; U.w1 = w1; U.s0 = s0; U.s1 = s1; U.in0 = in0; U.in1 = in1; U.idx = idx;
-    U.out0 = out0; U.out1 = out1; U.R = R; U.K = K; U.ldw = K; U.ldin = ldin; U.ldout = ldout;
-    U.ntok = ntok; U.tile_begin = tile_begin; U.epi = epi; U.out_f32 = out_f32; U.pad_ = 0;
-    return U;
-  };
   const deamoe_weights &W = a.w;
-  if (a.plan == PLAN_SLICE) {
+  if (slice) {
     const int ta_d = (a.d_s + kTile - 1) / kTile, ta_p = (a.d_p + kTile - 1) / kTile;
+    const int gd = tiles_per_item(a.d_s), gp = a.d_p ? tiles_per_item(a.d_p) : 1;
+    const int gse = a.d_se ? tiles_per_item(a.d_se) : 1;
+    const int bd = items_of(a.h, gd), bp = items_of(a.h, gp), bse = items_of(a.h, gse);
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_dcnt[j];
       const int32_t *idx = a.r.dept_tokens + my_doff;
       char *ao = static_cast<char *>(a.abuf_dept) + (size_t)my_doff * a.d_s * ab;
-      a.units[0][u] = make(wptr(W.dept_gate, j, a.d_s, a.h), wptr(W.dept_up, j, a.d_s, a.h),
-                           sptr(W.scale[0], j, a.d_s, a.h), sptr(W.scale[1], j, a.d_s, a.h), x, x,
-                           idx, ao, nullptr, a.d_s, a.h, a.h, a.d_s, my_dc, u * ta_d, EPI_SWIGLU,
-                           a.act_f32);
-      a.units[1][u] = make(wptr(W.dept_down, j, a.h, a.d_s), nullptr, sptr(W.scale[2], j, a.h, a.d_s),
-                           nullptr, ao, ao, nullptr, a.partial + (size_t)my_doff * a.h, nullptr,
-                           a.h, a.d_s, a.d_s, a.h, my_dc, u * th, EPI_STORE, 1);
+      put_unit(&a.units[0][u], wptr(W.dept_gate, j, a.d_s, a.h), wptr(W.dept_up, j, a.d_s, a.h),
+               sptr(W.scale[0], j, a.d_s, a.h), sptr(W.scale[1], j, a.d_s, a.h), x, x, idx, ao,
+               nullptr, a.d_s, a.h, a.h, a.d_s, my_dc, u * ta_d, EPI_SWIGLU, a.act_f32);
+      put_unit(&a.units[1][u], wptr(W.dept_down, j, a.h, a.d_s), nullptr,
+               sptr(W.scale[2], j, a.h, a.d_s), nullptr, ao, ao, nullptr,
+               a.partial + (size_t)my_doff * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, my_dc, u * bd,
+               EPI_STORE, 1, gd);
     }
-    for (int q = 0; q < 2; ++q) {
-      const int e = tid + q * kRouteThreads;
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      const int e = tid + q * BT;
       if (!has_priv || e >= n || my_ec[q] == 0) continue;
       const int u = ud + s_ecnt[e];
       const int32_t *idx = a.r.exp_tokens + my_eoff[q];
       char *ao = static_cast<char *>(a.abuf_exp) + (size_t)my_eoff[q] * a.d_p * ab;
-      a.units[0][u] = make(wptr(W.priv_gate, e, a.d_p, a.h), wptr(W.priv_up, e, a.d_p, a.h),
-                           sptr(W.scale[3], e, a.d_p, a.h), sptr(W.scale[4], e, a.d_p, a.h), x, x,
-                           idx, ao, nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q],
-                           ud * ta_d + s_ecnt[e] * ta_p, EPI_SWIGLU, a.act_f32);
-      a.units[1][u] = make(wptr(W.priv_down, e, a.h, a.d_p), nullptr, sptr(W.scale[5], e, a.h, a.d_p),
-                           nullptr, ao, ao, nullptr, a.partial + (size_t)(ndp + my_eoff[q]) * a.h,
-                           nullptr, a.h, a.d_p, a.d_p, a.h, my_ec[q], u * th, EPI_STORE, 1);
+      put_unit(&a.units[0][u], wptr(W.priv_gate, e, a.d_p, a.h), wptr(W.priv_up, e, a.d_p, a.h),
+               sptr(W.scale[3], e, a.d_p, a.h), sptr(W.scale[4], e, a.d_p, a.h), x, x, idx, ao,
+               nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q], ud * ta_d + s_ecnt[e] * ta_p,
+               EPI_SWIGLU, a.act_f32);
+      put_unit(&a.units[1][u], wptr(W.priv_down, e, a.h, a.d_p), nullptr,
+               sptr(W.scale[5], e, a.h, a.d_p), nullptr, ao, ao, nullptr,
+               a.partial + (size_t)(ndp + my_eoff[q]) * a.h, nullptr, a.h, a.d_p, a.d_p, a.h,
+               my_ec[q], ud * bd + s_ecnt[e] * bp, EPI_STORE, 1, gp);
     }
     if (tid == 0) {
       int units = ud + ue, tiles_a = ud * ta_d + ue * ta_p;
       if (has_se) {
         const int ta_se = (a.d_se + kTile - 1) / kTile;
-        a.units[0][units] = make(W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
-                                 sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr,
-                                 a.d_se, a.h, a.h, a.d_se, T, tiles_a, EPI_SWIGLU, a.act_f32);
-        a.units[1][units] = make(W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se), nullptr,
-                                 a.abuf_se, a.abuf_se, nullptr,
-                                 a.partial + (size_t)(ndp + nep_priv) * a.h, nullptr, a.h, a.d_se,
-                                 a.d_se, a.h, T, units * th, EPI_STORE, 1);
+        put_unit(&a.units[0][units], W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
+                 sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
+                 a.h, a.d_se, T, tiles_a, EPI_SWIGLU, a.act_f32);
+        put_unit(&a.units[1][units], W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se), nullptr,
+                 a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)(ndp + nep_priv) * a.h,
+                 nullptr, a.h, a.d_se, a.d_se, a.h, T, ud * bd + ue * bp, EPI_STORE, 1, gse);
         tiles_a += ta_se;
         ++units;
       }
       a.counts->stage[0][0] = units;
       a.counts->stage[0][1] = tiles_a;
       a.counts->stage[1][0] = units;
-      a.counts->stage[1][1] = units * th;
+      a.counts->stage[1][1] = ud * bd + ue * bp + (has_se ? bse : 0);
     }
   } else {  // PLAN_FACTORED
     const int d = a.d_s, td = (d + kTile - 1) / kTile;
+    const int gd = tiles_per_item(d), gse = a.d_se ? tiles_per_item(a.d_se) : 1;
+    const int bd = items_of(a.h, gd), bse = items_of(a.h, gse);
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_dcnt[j];
       const int32_t *idx = a.r.dept_tokens + my_doff;
       char *go = static_cast<char *>(a.gbuf) + (size_t)my_doff * d * ab;
       char *uo = static_cast<char *>(a.ubuf) + (size_t)my_doff * d * ab;
       char *zs = static_cast<char *>(a.zsbuf) + (size_t)my_doff * d * ab;
-      a.units[0][u] = make(wptr(W.dept_gate, j, d, a.h), wptr(W.dept_up, j, d, a.h),
-                           sptr(W.scale[0], j, d, a.h), sptr(W.scale[1], j, d, a.h), x, x, idx, go,
-                           uo, d, a.h, a.h, d, my_dc, u * td, EPI_SIGMA2, a.act_f32);
-      a.units[3][u] = make(wptr(W.dept_down, j, a.h, d), nullptr, sptr(W.scale[2], j, a.h, d),
-                           nullptr, zs, zs, nullptr, a.partial + (size_t)my_doff * a.h, nullptr,
-                           a.h, d, d, a.h, my_dc, u * th, EPI_STORE, 1);
+      put_unit(&a.units[0][u], wptr(W.dept_gate, j, d, a.h), wptr(W.dept_up, j, d, a.h),
+               sptr(W.scale[0], j, d, a.h), sptr(W.scale[1], j, d, a.h), x, x, idx, go, uo, d,
+               a.h, a.h, d, my_dc, u * td, EPI_SIGMA2, a.act_f32);
+      put_unit(&a.units[3][u], wptr(W.dept_down, j, a.h, d), nullptr, sptr(W.scale[2], j, a.h, d),
+               nullptr, zs, zs, nullptr, a.partial + (size_t)my_doff * a.h, nullptr, a.h, d, d,
+               a.h, my_dc, u * bd, EPI_STORE, 1, gd);
     }
-    for (int q = 0; q < 2; ++q) {
-      const int e = tid + q * kRouteThreads;
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      const int e = tid + q * BT;
       if (e >= n || my_ec[q] == 0) continue;
       const int u = s_ecnt[e];
       char *yo = static_cast<char *>(a.ybuf) + (size_t)my_eoff[q] * d * ab;
-      a.units[1][u] = make(wptr(W.priv_gate, e, d, d), wptr(W.priv_up, e, d, d),
-                           sptr(W.scale[3], e, d, d), sptr(W.scale[4], e, d, d), a.gbuf, a.ubuf,
-                           a.exp_src + my_eoff[q], yo, nullptr, d, d, d, d, my_ec[q], u * td,
-                           EPI_SWIGLU, a.act_f32);
-      a.units[2][u] = make(wptr(W.priv_down, e, d, d), nullptr, sptr(W.scale[5], e, d, d), nullptr,
-                           yo, yo, nullptr, a.zbuf + (size_t)my_eoff[q] * d, nullptr, d, d, d, d,
-                           my_ec[q], u * td, EPI_SIGMA, 1);
+      put_unit(&a.units[1][u], wptr(W.priv_gate, e, d, d), wptr(W.priv_up, e, d, d),
+               sptr(W.scale[3], e, d, d), sptr(W.scale[4], e, d, d), a.gbuf, a.ubuf,
+               a.exp_src + my_eoff[q], yo, nullptr, d, d, d, d, my_ec[q], u * td, EPI_SWIGLU,
+               a.act_f32);
+      put_unit(&a.units[2][u], wptr(W.priv_down, e, d, d), nullptr, sptr(W.scale[5], e, d, d),
+               nullptr, yo, yo, nullptr, a.zbuf + (size_t)my_eoff[q] * d, nullptr, d, d, d, d,
+               my_ec[q], u * td, EPI_SIGMA, 1);
     }
     if (tid == 0) {
       int units0 = ud, tiles0 = ud * td, units3 = ud;
       if (has_se) {
         const int ta_se = (a.d_se + kTile - 1) / kTile;
-        a.units[0][units0] = make(W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
-                                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se,
-                                  nullptr, a.d_se, a.h, a.h, a.d_se, T, tiles0, EPI_SWIGLU,
-                                  a.act_f32);
-        a.units[3][units3] = make(W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se), nullptr,
-                                  a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)ndp * a.h,
-                                  nullptr, a.h, a.d_se, a.d_se, a.h, T, units3 * th, EPI_STORE, 1);
+        put_unit(&a.units[0][units0], W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
+                 sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
+                 a.h, a.d_se, T, tiles0, EPI_SWIGLU, a.act_f32);
+        put_unit(&a.units[3][units3], W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
+                 nullptr, a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)ndp * a.h, nullptr,
+                 a.h, a.d_se, a.d_se, a.h, T, ud * bd, EPI_STORE, 1, gse);
         ++units0;
         tiles0 += ta_se;
         ++units3;
@@ -484,42 +562,25 @@ __global__ __launch_bounds__(kRouteThreads) void route_plan_kernel(RouteArgs a) 
       a.counts->stage[2][0] = ue;
       a.counts->stage[2][1] = ue * td;
       a.counts->stage[3][0] = units3;
-      a.counts->stage[3][1] = units3 * th;
+      a.counts->stage[3][1] = ud * bd + (has_se ? bse : 0);
     }
   }
   if (tid == 0) {
     a.counts->n_dept_pairs = ndp;
     a.counts->n_exp_pairs = nep_priv;
-    a.counts->n_pairs = ndp + (a.plan == PLAN_SLICE ? nep_priv : 0) + (has_se ? T : 0);
-  }
-  // combine slots of every token: its departments (ascending), then (SLICE)
-  // its experts in rank order, then the shared expert
-  for (int t = tid; t < T; t += kRouteThreads) {
-    int ns = 0;
-    int32_t *sp = a.slot_pair + (size_t)t * a.max_slots;
-    float *sw = a.slot_w + (size_t)t * a.max_slots;
-    for (int r = 0; r < s_nd[t]; ++r) {
-      sp[ns] = s_pair[t * k + r];
-      sw[ns] = a.plan == PLAN_SLICE ? s_dw[t * k + r] : 1.0f;
-      ++ns;
-    }
-    if (a.plan == PLAN_SLICE && a.d_p > 0)
-      for (int r = 0; r < k; ++r) {
-        sp[ns] = ndp + a.tok_exp_pair[t * k + r];
-        sw[ns] = s_w[t * k + r];
-        ++ns;
-      }
-    if (has_se) {
-      sp[ns] = ndp + (a.plan == PLAN_SLICE ? nep_priv : 0) + t;
-      sw[ns] = 1.0f;
-      ++ns;
-    }
-    a.nslot[t] = ns;
+    a.counts->n_pairs = ndp + (slice ? nep_priv : 0) + (has_se ? T : 0);
   }
 }
 
 hipError_t launch_route_plan(const RouteArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL(route_plan_kernel, dim3(1), dim3(kRouteThreads), 0, s, a);
+  // more logits per lane need more registers: half the threads from 513 experts on
+  const dim3 g(1);
+  if (a.n <= 64) hipLaunchKernelGGL((route_plan_kernel<1, 1024>), g, dim3(1024), 0, s, a);
+  else if (a.n <= 128) hipLaunchKernelGGL((route_plan_kernel<2, 1024>), g, dim3(1024), 0, s, a);
+  else if (a.n <= 256) hipLaunchKernelGGL((route_plan_kernel<4, 1024>), g, dim3(1024), 0, s, a);
+  else if (a.n <= 512) hipLaunchKernelGGL((route_plan_kernel<8, 1024>), g, dim3(1024), 0, s, a);
+  else if (a.n <= 1024) hipLaunchKernelGGL((route_plan_kernel<16, 512>), g, dim3(512), 0, s, a);
+  else hipLaunchKernelGGL((route_plan_kernel<32, 512>), g, dim3(512), 0, s, a);
   return hipGetLastError();
 }
 
