@@ -64,7 +64,7 @@ Layout make_layout(const deamoe_config &c) {
     return o;
   };
   L.logits = take(T * n * 4);
-  L.part = take((size_t)L.kc * T * n * 4);
+  L.part = take((size_t)L.kc * T * 64 * route_ns(c.n_experts) * 4);
   L.topk_ids = take(T * k * 4);
   L.topk_w = take(T * k * 4);
   L.tok_depts = take(T * k * 4);
@@ -197,6 +197,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
     ra.T = T;
     ra.kchunk = c.hidden / L.kc;
     ra.tiles = (c.n_experts + kTile - 1) / kTile;
+    ra.ldp = 64 * route_ns(c.n_experts);
     DEAMOE_TRY(launch_router(ra, c.act_dtype == DEAMOE_F32 ? WT_F32 : WT_BF16, ntt_of(T), L.kc, s));
     DEAMOE_TRY(ev.mark());
   }
@@ -219,6 +220,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.plan = plan;
   a.part = at<float>(ws, L.part);
   a.kc = L.kc;
+  a.ldp = 64 * route_ns(c.n_experts);
   a.logits_in = logits_in;
   a.bias = bias;
   a.r = r;
@@ -241,7 +243,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.zsbuf = at<void>(ws, L.zsbuf);
   a.zbuf = at<float>(ws, L.zbuf);
   a.partial = at<float>(ws, L.partial);
-  DEAMOE_TRY(launch_route_plan(a, s));
+  DEAMOE_TRY(launch_route(a, s));
   DEAMOE_TRY(ev.mark());
   return DEAMOE_OK;
 }
@@ -321,7 +323,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, false, ntt, 4, ta, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
-    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 1, false, ntt, 1, tiles_bound(units, c.hidden), kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 1, false, ntt, DEAMOE_KS_DOWN,
+                                   tiles_bound(units, c.hidden), kGridCap, s));
     DEAMOE_TRY(ev.mark());
   } else {
     const int d = c.d_shared;
@@ -348,7 +351,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     za.act_f32 = c.act_dtype == DEAMOE_F32;
     DEAMOE_TRY(launch_zsum(za, T * dk, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(3), wt, 1, false, ntt, 1,
+    DEAMOE_TRY(launch_grouped_gemm(stage(3), wt, 1, false, ntt, DEAMOE_KS_DOWN,
                                    tiles_bound(act_depts + se, c.hidden), kGridCap, s));
     DEAMOE_TRY(ev.mark());
   }

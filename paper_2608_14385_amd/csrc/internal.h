@@ -13,6 +13,12 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
+// K split of the down-projection stages (1: one wave per work item of
+// several row tiles; 2 or 4: the waves of a workgroup share one row tile).
+#ifndef DEAMOE_KS_DOWN
+#define DEAMOE_KS_DOWN 1
+#endif
+
 constexpr int kWave = 64;
 constexpr int kTile = 16;   // MFMA tile edge: 16 weight rows x 16 tokens
 

@@ -18,9 +18,17 @@ constexpr int kMaxMGrouped = 64;   // departments when top_k_dept > 0
 struct RouterArgs {
   const void *w;        // [n, h] act dtype
   const void *x;        // [T, h] act dtype
-  float *part;          // [kc, T, n]
-  int32_t n, h, T, kchunk, tiles;
+  float *part;          // [kc, T, ldp]
+  int32_t n, h, T, kchunk, tiles, ldp;
 };
+
+// Logits per lane of the per-token routing kernel (expert e = lane * NS + s);
+// the router's partial rows are padded to 64 * NS values.
+inline int route_ns(int n) {
+  int ns = 1;
+  while (64 * ns < n) ns *= 2;
+  return ns;
+}
 
 enum PlanMode : int32_t { PLAN_NONE = 0, PLAN_SLICE = 1, PLAN_FACTORED = 2 };
 
@@ -31,7 +39,7 @@ struct RouteArgs {
   int32_t h, d_s, d_p, d_se, act_f32, w_bytes, fp8, plan;
   // logits: sum of kc partial products, or injected; optional bias
   const float *part;
-  int32_t kc;
+  int32_t kc, ldp;
   const float *logits_in, *bias;
   // routing outputs
   deamoe_routing r;
@@ -67,7 +75,8 @@ struct ZsumArgs {
 };
 
 hipError_t launch_router(const RouterArgs &a, int wtype, int ntt, int kc, hipStream_t s);
-hipError_t launch_route_plan(const RouteArgs &a, hipStream_t s);
+// The per-token kernel (grid T) followed by the plan kernel (one workgroup).
+hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 // split: the stage's two matrices read different token operands (in0 / in1).
 hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, bool split, int ntt,
                                int ks, int max_tiles, int grid_cap, hipStream_t s);

@@ -3,17 +3,16 @@
 //
 // router_kernel: the logits W_r x as a grouped skinny product, split over KC
 //   chunks of the hidden dimension so that the n x h router matrix is read by
-//   many workgroups; each chunk's partial logits go to part[c][t][e].
-// route_plan_kernel: one workgroup of 1024 threads.
-//   phase 1, one wave per token: logits = sum of the KC partials in chunk
-//     order (+ bias, one fp32 add), optional group-limited department choice,
-//     top-k by (logit desc, id asc) with wavefront arg-max reductions, the
-//     routing weights, and the token's distinct departments with P_{t,j};
-//   phase 2: per-department and per-expert token lists in ascending token
-//     order (counts by scanning, offsets by a block-wide prefix sum, no
-//     atomics on any order-sensitive value);
-//   phase 3: the unit tables of every expert stage (pointers, row-tile
-//     prefix), the combine slots of every token, and the counts.
+//   many workgroups; each chunk's partial logits go to part[c][t][e] (rows
+//   padded to 64 * NS values).
+// route_token_kernel: one wave per token: logits = sum of the KC partials in
+//   chunk order (+ bias, one fp32 add), optional group-limited department
+//   choice, top-k by (logit desc, id asc), the routing weights, and the
+//   token's distinct departments with P_{t,j}.
+// plan_kernel: one workgroup: per-department and per-expert token lists in
+//   ascending token order (no atomics on any order-sensitive value), the
+//   unit tables of every expert stage (pointers, row-tile prefix), the
+//   combine slots of every token, and the counts.
 #include "gemm_tile.h"
 #include "launch.h"
 
@@ -31,12 +30,12 @@ __global__ __launch_bounds__(256) void router_kernel(RouterArgs a) {
   U.w0 = static_cast<const char *>(a.w) + (size_t)c * a.kchunk * Tr::W_BYTES;
   U.in0 = U.in1 = static_cast<const char *>(a.x) + (size_t)c * a.kchunk * Tr::A_BYTES;
   U.idx = nullptr;
-  U.out0 = a.part + (size_t)c * a.T * a.n;
+  U.out0 = a.part + (size_t)c * a.T * a.ldp;
   U.R = a.n;
   U.K = a.kchunk;
   U.ldw = a.h;
   U.ldin = a.h;
-  U.ldout = a.n;
+  U.ldout = a.ldp;
   U.ntok = a.T;
   U.epi = EPI_STORE;
   U.out_f32 = 1;
@@ -189,7 +188,9 @@ __device__ inline void put_unit(GemmUnit *U, const void *w0, const void *w1, con
 
 // Row tiles per work item of a stage whose K is not split across waves: short
 // contractions take several tiles so that a work item streams enough bytes.
-__device__ inline int tiles_per_item(int K) { return max(1, min(8, 2048 / K)); }
+__device__ inline int tiles_per_item(int K) {
+  return DEAMOE_KS_DOWN > 1 ? 1 : max(1, min(8, 2048 / K));
+}
 __device__ inline int items_of(int R, int tpg) { return ((R + kTile - 1) / kTile + tpg - 1) / tpg; }
 
 __device__ inline bool bit_at(const uint32_t *row, int i) { return (row[i >> 5] >> (i & 31)) & 1; }
@@ -204,181 +205,308 @@ __device__ inline int rank_below(const uint32_t *row, int i) {
 constexpr int kTW = kMaxT / 32;   // words of a token bitmap
 constexpr int kDW = kMaxM / 32;   // words of a department bitmap
 
-// NS: logits held per lane (n <= 64 * NS); BT: threads of the workgroup.
-//
-// Membership is kept as bitmaps in LDS: for every expert and department the
-// set of its tokens (kTW words), for every token the set of its departments.
-// A token's position in a CSR list is then the offset of the list plus the
-// number of member tokens below it, so every (token, rank) pair is placed
-// independently and the lists come out in ascending token order.
-template <int NS, int BT>
-__global__ __launch_bounds__(BT) void route_plan_kernel(RouteArgs a) {
-  constexpr int EPT = kMaxN / BT;   // experts per thread in the per-expert loops
-  __shared__ int32_t s_ids[kMaxTK];            // [t][rank] selected expert
-  __shared__ int32_t s_dep[kMaxTK];            // [t][slot] departments, ascending
-  __shared__ uint32_t s_etok[kMaxN * kTW];     // [e] token bitmap
-  __shared__ uint32_t s_dtok[kMaxM * kTW];     // [j] token bitmap
-  __shared__ uint32_t s_dbits[kMaxT * kDW];    // [t] department bitmap
-  __shared__ int32_t s_dcnt[kMaxM + 1];
-  __shared__ int32_t s_ecnt[kMaxN + 1];
-  __shared__ int32_t s_nd[kMaxT];
-  __shared__ int32_t s_gs[BT / 64][kMaxMGrouped];
-  __shared__ int32_t s_tmp[64];
+// NS consecutive fp32 values at p (aligned to 4 * NS bytes up to 16).
+template <int NS>
+__device__ inline void load_run(const float *p, float (&v)[NS]) {
+  if constexpr (NS == 1) {
+    v[0] = *p;
+  } else if constexpr (NS == 2) {
+    const float2 q = *reinterpret_cast<const float2 *>(p);
+    v[0] = q.x;
+    v[1] = q.y;
+  } else {
+#pragma unroll
+    for (int i = 0; i < NS / 4; ++i) {
+      const f32x4 q = *reinterpret_cast<const f32x4 *>(p + 4 * i);
+      v[4 * i] = q[0];
+      v[4 * i + 1] = q[1];
+      v[4 * i + 2] = q[2];
+      v[4 * i + 3] = q[3];
+    }
+  }
+}
 
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int T = a.T, n = a.n, m = a.m, k = a.k, E = a.E;
-  const int tw = (T + 31) / 32, dwords = (m + 31) / 32;
+__device__ inline int popc64(uint64_t v) { return __popcll(v); }
+
+// One wave per token (grid = T): logits, optional group limit, top-k,
+// routing weights and the token's distinct departments with P_{t,j}; the
+// token's combine slots when a plan follows.
+//
+// Top-k works on order keys (a monotone map of the logit to an unsigned
+// int).  A threshold is found by radix selection (built bit by bit from the
+// top; a bit stays if at least k keys reach the value), first over the
+// per-lane maxima; the few candidates at or above it rank themselves by
+// (logit desc, id asc) through LDS.
+template <int NS>
+__global__ __launch_bounds__(64) void route_token_kernel(RouteArgs a) {
+  __shared__ uint64_t s_sel[64];                // candidates in expert order
+  __shared__ uint64_t s_ord[kMaxK];             // winners in rank order
+  __shared__ int32_t s_gs[kMaxMGrouped];        // department scores (group limit)
+  __shared__ uint32_t s_db[kDW];                // the token's department bitmap
+  const int t = blockIdx.x, lane = threadIdx.x;
+  const int n = a.n, k = a.k, E = a.E, m = a.m;
+  const int dwords = (m + 31) / 32;
+  const int e0 = lane * NS;
+  if (lane < dwords) s_db[lane] = 0;
+
+  float lv[NS];
+  {
+    float l[NS];
+    if (a.logits_in) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) l[s] = a.logits_in[(size_t)t * n + min(e0 + s, n - 1)];
+    } else {
+      // partial sums of the router chunks, added in chunk order; loads of a
+      // batch are issued together (chunks past kc re-read the last one)
+      constexpr int CB = NS >= 4 ? 64 / NS : 16;
+      const float *p = a.part + (size_t)t * a.ldp + e0;
+      const size_t cs = (size_t)a.T * a.ldp;
+      for (int c0 = 0; c0 < a.kc; c0 += CB) {
+        float pc[CB][NS];
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) load_run<NS>(p + (size_t)min(c0 + cb, a.kc - 1) * cs, pc[cb]);
+        // selects, not branches: a branch here would serialize the loads
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {
+          const int c = c0 + cb;
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            const float sum = l[s] + pc[cb][s];
+            l[s] = c == 0 ? pc[cb][s] : (c < a.kc ? sum : l[s]);
+          }
+        }
+      }
+    }
+    if (a.bias) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) l[s] = l[s] + a.bias[min(e0 + s, n - 1)];
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      if (e0 + s < n) a.r.logits[(size_t)t * n + e0 + s] = l[s];
+      lv[s] = (e0 + s < n && l[s] == l[s]) ? l[s] : -INFINITY;   // NaN ranks last
+    }
+  }
+
+  // group-limited top-k: keep the kdept departments with the largest maximum
+  // logit (ties to the lower department id)
+  uint64_t keep = ~0ull;
+  if (a.kdept > 0) {
+    if (lane < m) s_gs[lane] = ord_key(-INFINITY);
+    wave_lds_sync();
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      if (e0 + s < n) atomicMax(&s_gs[(e0 + s) / E], ord_key(lv[s]));
+    wave_lds_sync();
+    const float gsv = lane < m ? ord_val(s_gs[lane]) : -INFINITY;
+    keep = 0;
+    for (int r = 0; r < a.kdept; ++r) {
+      float bv;
+      const int bj = wave_argmax_idx(gsv, lane, lane < m && !((keep >> lane) & 1), bv);
+      keep |= 1ull << (bj & 63);
+    }
+  }
+
+  // order keys; experts that may not be chosen get 0, below every eligible
+  // key (the key of -inf is 0x007fffff)
+  uint32_t key[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int e = e0 + s;
+    const bool ok = e < n && (a.kdept == 0 || ((keep >> ((e / E) & 63)) & 1));
+    key[s] = ok ? ord_u32(lv[s]) : 0u;
+  }
+  // Candidates.  theta, the k-th largest of the per-lane maxima, bounds the
+  // k-th largest key from below (k lanes hold a key >= theta), so every
+  // winner has a key >= theta; usually only a few keys reach it.  When more
+  // than 64 do, the exact k-th largest key tau is found by radix selection
+  // and the candidates are exactly the k winners.
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  uint32_t lmax = 0;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) lmax = max(lmax, key[s]);
+  uint32_t theta = 0;
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t cand = theta | (1u << b);
+    if (popc64(__ballot(lmax >= cand)) >= k) theta = cand;
+  }
+  int ncand = 0;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) ncand += popc64(__ballot(key[s] >= theta));
+  uint32_t selbits = 0;
+  if (ncand <= 64) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) selbits |= (uint32_t)(key[s] >= theta) << s;
+  } else {
+    uint32_t tau = 0;
+    for (int b = 31; b >= 0; --b) {
+      const uint32_t cand = tau | (1u << b);
+      int cnt = 0;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) cnt += popc64(__ballot(key[s] >= cand));
+      if (cnt >= k) tau = cand;
+    }
+    // keys above tau are fewer than k; the rest come from the keys equal to
+    // tau in ascending expert order (lanes first, then s)
+    int cnt_gt = 0, ties = 0;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      cnt_gt += popc64(__ballot(key[s] > tau));
+      ties += popc64(__ballot(key[s] == tau) & below);
+    }
+    const int need = k - cnt_gt;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const bool eq = key[s] == tau;
+      if (key[s] > tau || (eq && ties < need)) selbits |= 1u << s;
+      ties += eq;
+    }
+    ncand = k;
+  }
+  // candidates to LDS in expert order, then each ranks itself by (key desc,
+  // expert asc); the k best land in rank order
+  int pos = 0;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) pos += popc64(__ballot((selbits >> s) & 1) & below);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    if ((selbits >> s) & 1) {
+      s_sel[pos] = ((uint64_t)key[s] << 32) | (uint32_t)~(uint32_t)(e0 + s);
+      ++pos;
+    }
+  }
+  wave_lds_sync();
+  if (lane < ncand) {
+    const uint64_t mine = s_sel[lane];
+    int rank = 0;
+    for (int j = 0; j < ncand; ++j) rank += s_sel[j] > mine;
+    if (rank < k) s_ord[rank] = mine;
+  }
+  wave_lds_sync();
+  const bool sel = lane < k;
+  const uint64_t kk = sel ? s_ord[lane] : 0ull;
+  const int my_id = sel ? (int)~(uint32_t)kk : 0;
+  const uint32_t ob = (uint32_t)(kk >> 32);
+  const float my_l = __uint_as_float((ob & 0x80000000u) ? (ob & 0x7fffffffu) : ~ob);
+
+  // routing weights
+  float p;
+  if (a.score == DEAMOE_SCORE_SOFTMAX) {
+    float mx, den;
+    if (a.renorm) {
+      mx = __shfl(my_l, 0);
+      den = wave_sum(sel ? expf(my_l - mx) : 0.f);
+    } else {
+      float lm = -INFINITY;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) lm = fmaxf(lm, lv[s]);
+      mx = wave_max(lm);
+      float ls = 0.f;
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        if (e0 + s < n) ls += expf(lv[s] - mx);
+      den = wave_sum(ls);
+    }
+    p = expf(my_l - mx) / den;
+  } else {
+    const float sg = 1.0f / (1.0f + expf(-my_l));
+    p = a.renorm ? sg / wave_sum(sel ? sg : 0.f) : sg;
+  }
+  p *= a.route_scale;
+  const int d = sel ? my_id / E : 0;
+  if (sel) {
+    a.r.topk_ids[t * k + lane] = my_id;
+    a.r.topk_w[t * k + lane] = p;
+    atomicOr(&s_db[d >> 5], 1u << (d & 31));
+  }
+  wave_lds_sync();
+  // distinct departments, ascending, each with the weights of its selected
+  // experts summed in rank order
+  int nd = 0;
+  for (int w = 0; w < dwords; ++w) nd += __popc(s_db[w]);
+  nd = __builtin_amdgcn_readfirstlane(nd);
+  float P = 0.f;
+  uint32_t eqm = 0;
+  for (int q = 0; q < k; ++q) {
+    const int dq = __builtin_amdgcn_readlane(d, q);
+    const float pq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), q));
+    if (dq == d) { P += pq; eqm |= 1u << q; }
+  }
+  const bool first = sel && (eqm & ((1u << lane) - 1u)) == 0;
   const bool slice = a.plan == PLAN_SLICE;
   const bool exp_slots = slice && a.d_p > 0;
   const int S = a.max_slots;
-  for (int i = tid; i < n * kTW; i += BT) s_etok[i] = 0;
-  for (int i = tid; i < m * kTW; i += BT) s_dtok[i] = 0;
-  for (int i = tid; i < T * dwords; i += BT) s_dbits[i] = 0;
-  __syncthreads();
-
-  // ------------------------------------------------ phase 1: one wave per token
-  for (int t = wave; t < T; t += BT / 64) {
-    float lv[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const int e = lane + 64 * s;
-      const int ec = e < n ? e : n - 1;
-      float l;
-      if (a.logits_in) {
-        l = a.logits_in[(size_t)t * n + ec];
-      } else {  // partial sums of the router chunks, added in chunk order; all
-                // loads are issued first (chunks past kc re-read the last one)
-        float pc[kMaxKC];
-#pragma unroll
-        for (int c = 0; c < kMaxKC; ++c)
-          pc[c] = a.part[((size_t)min(c, a.kc - 1) * T + t) * n + ec];
-        l = pc[0];
-#pragma unroll
-        for (int c = 1; c < kMaxKC; ++c) l = c < a.kc ? l + pc[c] : l;
-      }
-      if (a.bias) l = l + a.bias[ec];
-      if (e < n) a.r.logits[(size_t)t * n + e] = l;
-      lv[s] = (e < n && l == l) ? l : -INFINITY;   // NaN ranks last
-    }
-    // group-limited top-k: keep the kdept departments with the largest
-    // maximum logit (ties to the lower department id)
-    uint64_t keep = ~0ull;
-    if (a.kdept > 0) {
-      if (lane < m) s_gs[wave][lane] = ord_key(-INFINITY);
-      wave_lds_sync();
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const int e = lane + 64 * s;
-        if (e < n) atomicMax(&s_gs[wave][e / E], ord_key(lv[s]));
-      }
-      wave_lds_sync();
-      const float gsv = lane < m ? ord_val(s_gs[wave][lane]) : -INFINITY;
-      keep = 0;
-      for (int r = 0; r < a.kdept; ++r) {
-        float bv;
-        const int bj = wave_argmax_idx(gsv, lane, lane < m && !((keep >> lane) & 1), bv);
-        keep |= 1ull << (bj & 63);
-      }
-    }
-    // top-k: k rounds of arg-max over the lane-held logits
-    uint32_t taken = 0;
-    int my_id = 0;
-    float my_l = -INFINITY;
-    for (int r = 0; r < k; ++r) {
-      float bv = -INFINITY;
-      int be = 0x7fffffff;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const int e = lane + 64 * s;
-        const bool ok = e < n && !((taken >> s) & 1) &&
-                        (a.kdept == 0 || ((keep >> ((e / E) & 63)) & 1));
-        if (ok && ranks_before(lv[s], e, bv, be)) { bv = lv[s]; be = e; }
-      }
-      be = wave_argmax_idx(bv, be, be != 0x7fffffff, bv);
-      if (be < 0 || be >= n) be = 0;   // unreachable: at least k experts are always eligible
-      if ((be & 63) == lane) taken |= 1u << (be >> 6);
-      if (lane == r) { my_id = be; my_l = bv; }
-    }
-    // routing weights
-    const bool sel = lane < k;
-    float p;
-    if (a.score == DEAMOE_SCORE_SOFTMAX) {
-      float mx, den;
-      if (a.renorm) {
-        mx = __shfl(my_l, 0);
-        den = wave_sum(sel ? expf(my_l - mx) : 0.f);
-      } else {
-        float lm = -INFINITY;
-#pragma unroll
-        for (int s = 0; s < NS; ++s) lm = fmaxf(lm, lv[s]);
-        mx = wave_max(lm);
-        float ls = 0.f;
-#pragma unroll
-        for (int s = 0; s < NS; ++s)
-          if (lane + 64 * s < n) ls += expf(lv[s] - mx);
-        den = wave_sum(ls);
-      }
-      p = expf(my_l - mx) / den;
-    } else {
-      const float sg = 1.0f / (1.0f + expf(-my_l));
-      p = a.renorm ? sg / wave_sum(sel ? sg : 0.f) : sg;
-    }
-    p *= a.route_scale;
-    const int d = sel ? my_id / E : 0;
-    if (sel) {
-      a.r.topk_ids[t * k + lane] = my_id;
-      a.r.topk_w[t * k + lane] = p;
-      s_ids[t * k + lane] = my_id;
-      atomicOr(&s_etok[my_id * kTW + (t >> 5)], 1u << (t & 31));
-      atomicOr(&s_dtok[d * kTW + (t >> 5)], 1u << (t & 31));
-      atomicOr(&s_dbits[t * dwords + (d >> 5)], 1u << (d & 31));
-    }
-    wave_lds_sync();
-    // distinct departments, ascending, each with the weights of its selected
-    // experts summed in rank order
-    const uint32_t *drow = s_dbits + t * dwords;
-    int nd = 0;
-    for (int w = 0; w < dwords; ++w) nd += __popc(drow[w]);
-    nd = __builtin_amdgcn_readfirstlane(nd);
-    float P = 0.f;
-    uint32_t eq = 0;
-    for (int q = 0; q < k; ++q) {
-      const int dq = __builtin_amdgcn_readlane(d, q);
-      const float pq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), q));
-      if (dq == d) { P += pq; eq |= 1u << q; }
-    }
-    const bool first = sel && (eq & ((1u << lane) - 1u)) == 0;
-    if (first) {
-      const int pos = rank_below(drow, d);
-      a.r.tok_depts[t * k + pos] = d;
-      a.r.tok_dept_w[t * k + pos] = P;
-      s_dep[t * k + pos] = d;
-      if (a.plan) a.slot_w[(size_t)t * S + pos] = slice ? P : 1.0f;
-    }
-    if (lane >= nd && lane < k) {
-      a.r.tok_depts[t * k + lane] = -1;
-      a.r.tok_dept_w[t * k + lane] = 0.f;
-    }
-    if (a.plan && exp_slots && sel) a.slot_w[(size_t)t * S + nd + lane] = p;
-    if (lane == 0) {
-      a.r.tok_ndept[t] = nd;
-      s_nd[t] = nd;
-      if (a.plan) {
-        const int ns = nd + (exp_slots ? k : 0);
-        if (a.d_se > 0) a.slot_w[(size_t)t * S + ns] = 1.0f;
-        a.nslot[t] = ns + (a.d_se > 0 ? 1 : 0);
-      }
+  if (first) {
+    const int dpos = rank_below(s_db, d);
+    a.r.tok_depts[t * k + dpos] = d;
+    a.r.tok_dept_w[t * k + dpos] = P;
+    if (a.plan) a.slot_w[(size_t)t * S + dpos] = slice ? P : 1.0f;
+  }
+  if (lane >= nd && lane < k) {
+    a.r.tok_depts[t * k + lane] = -1;
+    a.r.tok_dept_w[t * k + lane] = 0.f;
+  }
+  if (a.plan && exp_slots && sel) a.slot_w[(size_t)t * S + nd + lane] = p;
+  if (lane == 0) {
+    a.r.tok_ndept[t] = nd;
+    if (a.plan) {
+      const int ns = nd + (exp_slots ? k : 0);
+      if (a.d_se > 0) a.slot_w[(size_t)t * S + ns] = 1.0f;
+      a.nslot[t] = ns + (a.d_se > 0 ? 1 : 0);
     }
   }
+}
+
+// One workgroup: the per-department and per-expert token lists (ascending
+// token order) from the per-token results, then the unit tables of every
+// expert stage and the combine slots.
+//
+// Membership is kept as token bitmaps in LDS for every expert and
+// department.  A token's position in a CSR list is the offset of the list
+// plus the number of member tokens below it, so every (token, rank) pair is
+// placed independently.  Counts and the number of active units are summed
+// in one scan over departments then experts, packed as count | active << 16
+// (both sums stay below 2^16).
+template <int BT>
+__global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
+  constexpr int EPT = kMaxN / BT;   // experts per thread in the per-expert loops
+  __shared__ int32_t s_ids[kMaxTK];            // [t][rank] selected expert
+  __shared__ int32_t s_dep[kMaxTK];            // [t][slot] departments, -1 padded
+  __shared__ uint32_t s_etok[kMaxN * kTW];     // [e] token bitmap
+  __shared__ uint32_t s_dtok[kMaxM * kTW];     // [j] token bitmap
+  __shared__ int32_t s_scan[kMaxM + kMaxN];    // [depts, experts] packed prefix
+  __shared__ int32_t s_nd[kMaxT];
+  __shared__ int32_t s_tmp[64];
+
+  const int tid = threadIdx.x;
+  const int T = a.T, n = a.n, m = a.m, k = a.k, E = a.E;
+  const int tw = (T + 31) / 32;
+  const bool slice = a.plan == PLAN_SLICE;
+  const bool exp_slots = slice && a.d_p > 0;
+  const bool has_priv = a.plan == PLAN_FACTORED || a.d_p > 0;
+  const bool has_se = a.d_se > 0;
+  const int S = a.max_slots;
+  for (int i = tid; i < n * kTW; i += BT) s_etok[i] = 0;
+  for (int i = tid; i < m * kTW; i += BT) s_dtok[i] = 0;
+  __syncthreads();
+  for (int idx = tid; idx < T * k; idx += BT) {
+    const int t = idx / k;
+    const uint32_t bit = 1u << (t & 31);
+    const int e = a.r.topk_ids[idx], j = a.r.tok_depts[idx];
+    s_ids[idx] = e;
+    s_dep[idx] = j;
+    atomicOr(&s_etok[e * kTW + (t >> 5)], bit);
+    if (j >= 0) atomicOr(&s_dtok[j * kTW + (t >> 5)], bit);
+  }
+  for (int t = tid; t < T; t += BT) s_nd[t] = a.r.tok_ndept[t];
   __syncthreads();
 
-  // ------------------------------------------------ phase 2: counts and lists
+  // counts
   int my_dc = 0, my_ec[EPT] = {};
   if (tid < m) {
     for (int w = 0; w < tw; ++w) my_dc += __popc(s_dtok[tid * kTW + w]);
-    s_dcnt[tid] = my_dc;
     a.r.dept_count[tid] = my_dc;
+    s_scan[tid] = my_dc | ((my_dc > 0) << 16);
   }
 #pragma unroll
   for (int q = 0; q < EPT; ++q) {
@@ -387,18 +515,19 @@ __global__ __launch_bounds__(BT) void route_plan_kernel(RouteArgs a) {
       int c = 0;
       for (int w = 0; w < tw; ++w) c += __popc(s_etok[e * kTW + w]);
       my_ec[q] = c;
-      s_ecnt[e] = c;
       a.r.exp_count[e] = c;
+      s_scan[m + e] = c | ((has_priv && c > 0) << 16);
     }
   }
   __syncthreads();
-  const int ndp = block_exscan(s_dcnt, m, s_tmp);
-  const int nep = block_exscan(s_ecnt, n, s_tmp);
-  const bool has_priv = a.plan == PLAN_FACTORED || a.d_p > 0;
-  const bool has_se = a.d_se > 0;
+  const int tot = block_exscan(s_scan, m + n, s_tmp);
+  const int ndp = s_scan[m] & 0xffff, ud = s_scan[m] >> 16;
+  const int nep = (tot & 0xffff) - ndp, ue = (tot >> 16) - ud;
   const int nep_priv = has_priv ? nep : 0;
-  if (tid < m) a.r.dept_offset[tid] = s_dcnt[tid];
-  for (int e = tid; e < n; e += BT) a.r.exp_offset[e] = s_ecnt[e];
+  auto doff = [&](int j) { return s_scan[j] & 0xffff; };
+  auto eoff = [&](int e) { return (s_scan[m + e] & 0xffff) - ndp; };
+  if (tid < m) a.r.dept_offset[tid] = doff(tid);
+  for (int e = tid; e < n; e += BT) a.r.exp_offset[e] = eoff(e);
   if (tid == 0) {
     a.r.dept_offset[m] = ndp;
     a.r.exp_offset[n] = nep;
@@ -408,47 +537,30 @@ __global__ __launch_bounds__(BT) void route_plan_kernel(RouteArgs a) {
   for (int idx = tid; idx < T * k; idx += BT) {
     const int t = idx / k, q = idx - t * k;
     const int e = s_ids[idx];
-    const int pe = s_ecnt[e] + rank_below(s_etok + e * kTW, t);
+    const int pe = eoff(e) + rank_below(s_etok + e * kTW, t);
     a.r.exp_tokens[pe] = t;
     if (a.plan) {
       a.tok_exp_pair[idx] = pe;
       if (exp_slots) a.slot_pair[(size_t)t * S + s_nd[t] + q] = ndp + pe;
       if (a.plan == PLAN_FACTORED) {
         const int j = e / E;
-        a.exp_src[pe] = s_dcnt[j] + rank_below(s_dtok + j * kTW, t);
+        a.exp_src[pe] = doff(j) + rank_below(s_dtok + j * kTW, t);
       }
     }
-    if (q < s_nd[t]) {
-      const int j = s_dep[idx];
-      const int pd = s_dcnt[j] + rank_below(s_dtok + j * kTW, t);
+    const int j = s_dep[idx];
+    if (j >= 0) {
+      const int pd = doff(j) + rank_below(s_dtok + j * kTW, t);
       a.r.dept_tokens[pd] = t;
       if (a.plan) a.slot_pair[(size_t)t * S + q] = pd;
     }
   }
-  if (a.plan && has_se)
+  if (!a.plan) return;
+  if (has_se)
     for (int t = tid; t < T; t += BT)
       a.slot_pair[(size_t)t * S + s_nd[t] + (exp_slots ? k : 0)] = ndp + (slice ? nep_priv : 0) + t;
-  if (!a.plan) return;
-  const int my_doff = tid < m ? s_dcnt[tid] : 0;
-  int my_eoff[EPT] = {};
-#pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    const int e = tid + q * BT;
-    if (e < n) my_eoff[q] = s_ecnt[e];
-  }
-  __syncthreads();
 
-  // ------------------------------------------------ phase 3: stage unit tables
-  // unit index of every active department / expert (prefix over active flags)
-  if (tid < m) s_dcnt[tid] = my_dc > 0;
-#pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    const int e = tid + q * BT;
-    if (e < n) s_ecnt[e] = has_priv && my_ec[q] > 0;
-  }
-  __syncthreads();
-  const int ud = block_exscan(s_dcnt, m, s_tmp);
-  const int ue = block_exscan(s_ecnt, n, s_tmp);
+  // unit tables: unit index of an active department / expert = number of
+  // active ones before it
   const int wb = a.w_bytes, ab = a.act_f32 ? 4 : 2;
   const char *x = static_cast<const char *>(a.x);
   auto wptr = [&](const void *base, int idx, int R, int C) -> const void * {
@@ -465,44 +577,43 @@ __global__ __launch_bounds__(BT) void route_plan_kernel(RouteArgs a) {
     const int gse = a.d_se ? tiles_per_item(a.d_se) : 1;
     const int bd = items_of(a.h, gd), bp = items_of(a.h, gp), bse = items_of(a.h, gse);
     if (tid < m && my_dc > 0) {
-      const int j = tid, u = s_dcnt[j];
-      const int32_t *idx = a.r.dept_tokens + my_doff;
-      char *ao = static_cast<char *>(a.abuf_dept) + (size_t)my_doff * a.d_s * ab;
+      const int j = tid, u = s_scan[j] >> 16, off = doff(j);
+      const int32_t *idx = a.r.dept_tokens + off;
+      char *ao = static_cast<char *>(a.abuf_dept) + (size_t)off * a.d_s * ab;
       put_unit(&a.units[0][u], wptr(W.dept_gate, j, a.d_s, a.h), wptr(W.dept_up, j, a.d_s, a.h),
                sptr(W.scale[0], j, a.d_s, a.h), sptr(W.scale[1], j, a.d_s, a.h), x, x, idx, ao,
                nullptr, a.d_s, a.h, a.h, a.d_s, my_dc, u * ta_d, EPI_SWIGLU, a.act_f32);
       put_unit(&a.units[1][u], wptr(W.dept_down, j, a.h, a.d_s), nullptr,
                sptr(W.scale[2], j, a.h, a.d_s), nullptr, ao, ao, nullptr,
-               a.partial + (size_t)my_doff * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, my_dc, u * bd,
+               a.partial + (size_t)off * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, my_dc, u * bd,
                EPI_STORE, 1, gd);
     }
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
       const int e = tid + q * BT;
       if (!has_priv || e >= n || my_ec[q] == 0) continue;
-      const int u = ud + s_ecnt[e];
-      const int32_t *idx = a.r.exp_tokens + my_eoff[q];
-      char *ao = static_cast<char *>(a.abuf_exp) + (size_t)my_eoff[q] * a.d_p * ab;
+      const int ui = (s_scan[m + e] >> 16) - ud, u = ud + ui, off = eoff(e);
+      const int32_t *idx = a.r.exp_tokens + off;
+      char *ao = static_cast<char *>(a.abuf_exp) + (size_t)off * a.d_p * ab;
       put_unit(&a.units[0][u], wptr(W.priv_gate, e, a.d_p, a.h), wptr(W.priv_up, e, a.d_p, a.h),
                sptr(W.scale[3], e, a.d_p, a.h), sptr(W.scale[4], e, a.d_p, a.h), x, x, idx, ao,
-               nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q], ud * ta_d + s_ecnt[e] * ta_p,
-               EPI_SWIGLU, a.act_f32);
+               nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q], ud * ta_d + ui * ta_p, EPI_SWIGLU,
+               a.act_f32);
       put_unit(&a.units[1][u], wptr(W.priv_down, e, a.h, a.d_p), nullptr,
                sptr(W.scale[5], e, a.h, a.d_p), nullptr, ao, ao, nullptr,
-               a.partial + (size_t)(ndp + my_eoff[q]) * a.h, nullptr, a.h, a.d_p, a.d_p, a.h,
-               my_ec[q], ud * bd + s_ecnt[e] * bp, EPI_STORE, 1, gp);
+               a.partial + (size_t)(ndp + off) * a.h, nullptr, a.h, a.d_p, a.d_p, a.h, my_ec[q],
+               ud * bd + ui * bp, EPI_STORE, 1, gp);
     }
     if (tid == 0) {
       int units = ud + ue, tiles_a = ud * ta_d + ue * ta_p;
       if (has_se) {
-        const int ta_se = (a.d_se + kTile - 1) / kTile;
         put_unit(&a.units[0][units], W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
                  a.h, a.d_se, T, tiles_a, EPI_SWIGLU, a.act_f32);
         put_unit(&a.units[1][units], W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se), nullptr,
                  a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)(ndp + nep_priv) * a.h,
                  nullptr, a.h, a.d_se, a.d_se, a.h, T, ud * bd + ue * bp, EPI_STORE, 1, gse);
-        tiles_a += ta_se;
+        tiles_a += (a.d_se + kTile - 1) / kTile;
         ++units;
       }
       a.counts->stage[0][0] = units;
@@ -515,36 +626,35 @@ __global__ __launch_bounds__(BT) void route_plan_kernel(RouteArgs a) {
     const int gd = tiles_per_item(d), gse = a.d_se ? tiles_per_item(a.d_se) : 1;
     const int bd = items_of(a.h, gd), bse = items_of(a.h, gse);
     if (tid < m && my_dc > 0) {
-      const int j = tid, u = s_dcnt[j];
-      const int32_t *idx = a.r.dept_tokens + my_doff;
-      char *go = static_cast<char *>(a.gbuf) + (size_t)my_doff * d * ab;
-      char *uo = static_cast<char *>(a.ubuf) + (size_t)my_doff * d * ab;
-      char *zs = static_cast<char *>(a.zsbuf) + (size_t)my_doff * d * ab;
+      const int j = tid, u = s_scan[j] >> 16, off = doff(j);
+      const int32_t *idx = a.r.dept_tokens + off;
+      char *go = static_cast<char *>(a.gbuf) + (size_t)off * d * ab;
+      char *uo = static_cast<char *>(a.ubuf) + (size_t)off * d * ab;
+      char *zs = static_cast<char *>(a.zsbuf) + (size_t)off * d * ab;
       put_unit(&a.units[0][u], wptr(W.dept_gate, j, d, a.h), wptr(W.dept_up, j, d, a.h),
                sptr(W.scale[0], j, d, a.h), sptr(W.scale[1], j, d, a.h), x, x, idx, go, uo, d,
                a.h, a.h, d, my_dc, u * td, EPI_SIGMA2, a.act_f32);
       put_unit(&a.units[3][u], wptr(W.dept_down, j, a.h, d), nullptr, sptr(W.scale[2], j, a.h, d),
-               nullptr, zs, zs, nullptr, a.partial + (size_t)my_doff * a.h, nullptr, a.h, d, d,
+               nullptr, zs, zs, nullptr, a.partial + (size_t)off * a.h, nullptr, a.h, d, d,
                a.h, my_dc, u * bd, EPI_STORE, 1, gd);
     }
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
       const int e = tid + q * BT;
       if (e >= n || my_ec[q] == 0) continue;
-      const int u = s_ecnt[e];
-      char *yo = static_cast<char *>(a.ybuf) + (size_t)my_eoff[q] * d * ab;
+      const int u = (s_scan[m + e] >> 16) - ud, off = eoff(e);
+      char *yo = static_cast<char *>(a.ybuf) + (size_t)off * d * ab;
       put_unit(&a.units[1][u], wptr(W.priv_gate, e, d, d), wptr(W.priv_up, e, d, d),
                sptr(W.scale[3], e, d, d), sptr(W.scale[4], e, d, d), a.gbuf, a.ubuf,
-               a.exp_src + my_eoff[q], yo, nullptr, d, d, d, d, my_ec[q], u * td, EPI_SWIGLU,
+               a.exp_src + off, yo, nullptr, d, d, d, d, my_ec[q], u * td, EPI_SWIGLU,
                a.act_f32);
       put_unit(&a.units[2][u], wptr(W.priv_down, e, d, d), nullptr, sptr(W.scale[5], e, d, d),
-               nullptr, yo, yo, nullptr, a.zbuf + (size_t)my_eoff[q] * d, nullptr, d, d, d, d,
+               nullptr, yo, yo, nullptr, a.zbuf + (size_t)off * d, nullptr, d, d, d, d,
                my_ec[q], u * td, EPI_SIGMA, 1);
     }
     if (tid == 0) {
       int units0 = ud, tiles0 = ud * td, units3 = ud;
       if (has_se) {
-        const int ta_se = (a.d_se + kTile - 1) / kTile;
         put_unit(&a.units[0][units0], W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
                  a.h, a.d_se, T, tiles0, EPI_SWIGLU, a.act_f32);
@@ -552,7 +662,7 @@ __global__ __launch_bounds__(BT) void route_plan_kernel(RouteArgs a) {
                  nullptr, a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)ndp * a.h, nullptr,
                  a.h, a.d_se, a.d_se, a.h, T, ud * bd, EPI_STORE, 1, gse);
         ++units0;
-        tiles0 += ta_se;
+        tiles0 += (a.d_se + kTile - 1) / kTile;
         ++units3;
       }
       a.counts->stage[0][0] = units0;
@@ -572,15 +682,19 @@ __global__ __launch_bounds__(BT) void route_plan_kernel(RouteArgs a) {
   }
 }
 
-hipError_t launch_route_plan(const RouteArgs &a, hipStream_t s) {
-  // more logits per lane need more registers: half the threads from 513 experts on
-  const dim3 g(1);
-  if (a.n <= 64) hipLaunchKernelGGL((route_plan_kernel<1, 1024>), g, dim3(1024), 0, s, a);
-  else if (a.n <= 128) hipLaunchKernelGGL((route_plan_kernel<2, 1024>), g, dim3(1024), 0, s, a);
-  else if (a.n <= 256) hipLaunchKernelGGL((route_plan_kernel<4, 1024>), g, dim3(1024), 0, s, a);
-  else if (a.n <= 512) hipLaunchKernelGGL((route_plan_kernel<8, 1024>), g, dim3(1024), 0, s, a);
-  else if (a.n <= 1024) hipLaunchKernelGGL((route_plan_kernel<16, 512>), g, dim3(512), 0, s, a);
-  else hipLaunchKernelGGL((route_plan_kernel<32, 512>), g, dim3(512), 0, s, a);
+hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
+  const dim3 g(a.T), b(64);
+  switch (route_ns(a.n)) {
+    case 1: hipLaunchKernelGGL((route_token_kernel<1>), g, b, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((route_token_kernel<2>), g, b, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((route_token_kernel<4>), g, b, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((route_token_kernel<8>), g, b, 0, s, a); break;
+    case 16: hipLaunchKernelGGL((route_token_kernel<16>), g, b, 0, s, a); break;
+    default: hipLaunchKernelGGL((route_token_kernel<32>), g, b, 0, s, a); break;
+  }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((plan_kernel<1024>), dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 

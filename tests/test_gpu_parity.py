@@ -14,6 +14,7 @@ import torch
 
 sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
 from gpu_util import Case, compare_outputs, compare_routing, sample_tokens, say  # noqa: E402
+import oracle  # noqa: E402
 from paper_2608_14385_amd import deamoe as D  # noqa: E402
 from paper_2608_14385_amd import workloads as W  # noqa: E402
 
@@ -158,6 +159,34 @@ def test_deterministic_and_route_only():
     h3 = rt.host()
     for k in h1:
         assert np.array_equal(h1[k], h3[k]), k
+
+
+@pytest.mark.parametrize("preset", ["tiny_f32", "7b_bf16", "dsv3_bf16", "dsv3_factored"])
+def test_route_ties(preset):
+    """Coarse injected logits: many exact ties, including every logit equal
+    (more candidates than one per lane, so the exact selection path runs) and
+    a few equal values at the top (the candidate path); the lower id wins."""
+    cfg = P[preset].layer
+    T, n = 12, cfg.n_experts
+    g = torch.Generator(device="cpu").manual_seed(5)
+    u = torch.rand(T, n, generator=g)
+    rows = [torch.full((n,), 0.5),                                  # all equal
+            torch.round(u[1] * 4) / 4,                              # five levels
+            torch.round(u[2] * 64) / 64,                            # 65 levels
+            torch.where(u[3] > 0.97, torch.tensor(2.0), u[3])]      # equal maxima
+    rows += [torch.round(u[t] * (1 + t)) / (1 + t) for t in range(4, T)]
+    logits = torch.stack(rows).to(torch.float32).contiguous()
+    act = torch.float32 if cfg.act_dtype == "f32" else torch.bfloat16
+    x = torch.zeros(T, cfg.hidden, dtype=act)
+    router = torch.zeros(n, cfg.hidden, dtype=act)
+    say(f"[gpu] route ties {preset} T={T}")
+    c = D.make_config(cfg, T)
+    ws = D.alloc_workspace(c)
+    rt = D.Routing.alloc(cfg, T)
+    D.deamoe_route(c, x.cuda(), router.cuda(), rt, ws, logits_in=logits.cuda())
+    torch.cuda.synchronize()
+    ref = oracle.route(cfg, x, router, logits_in=logits, bias=None, T=T)
+    compare_routing(rt.host(), ref, T, cfg.top_k)
 
 
 def test_empty_batch_is_a_no_op():
