@@ -156,6 +156,10 @@ int validate_weights(const deamoe_config &c, const deamoe_weights *w, bool need_
 
 int ntt_of(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
 
+// Rows of a down-projection tile: row pairs while the token tiles are few
+// enough for both halves' accumulators to stay in registers.
+int down_rows_of(int T) { return DEAMOE_DOWN_PAIR && ntt_of(T) <= 2 ? 2 * kTile : kTile; }
+
 template <class P>
 P *at(void *ws, size_t off) {
   return reinterpret_cast<P *>(static_cast<char *>(ws) + off);
@@ -218,6 +222,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.w_bytes = wbytes_of(c.w_dtype);
   a.fp8 = c.w_dtype == DEAMOE_FP8_E4M3_B128;
   a.plan = plan;
+  a.down_rows = down_rows_of(T);
   a.part = at<float>(ws, L.part);
   a.kc = L.kc;
   a.ldp = 64 * route_ns(c.n_experts);
@@ -276,7 +281,18 @@ bool routing_complete(const deamoe_routing &r) {
 }
 
 // Upper bound of the row tiles of a stage, for the grid size.
-int tiles_bound(int units_max, int R) { return units_max * ((R + kTile - 1) / kTile); }
+int tiles_bound(int units_max, int R, int rows = kTile) {
+  return units_max * ((R + rows - 1) / rows);
+}
+
+// Launch of a down-projection stage (K split DEAMOE_KS_DOWN).
+hipError_t launch_down(const GemmStage &st, int wt, int T, int units_max, int R, int cap,
+                       hipStream_t s) {
+  const int rows = down_rows_of(T);
+  const bool pair = rows == 2 * kTile;
+  return launch_grouped_gemm(st, wt, pair ? 2 : 1, pair ? GEMM_PAIR : GEMM_PLAIN, ntt_of(T),
+                             DEAMOE_KS_DOWN, tiles_bound(units_max, R, rows), cap, s);
+}
 
 constexpr int kGridCap = 8192;   // 256 CUs x 32 workgroups
 
@@ -320,20 +336,21 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     const int ta = tiles_bound(act_depts, c.d_shared) +
                    (c.d_private ? tiles_bound(act_exps, c.d_private) : 0) +
                    se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, false, ntt, 4, ta, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, ta, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
-    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 1, false, ntt, DEAMOE_KS_DOWN,
-                                   tiles_bound(units, c.hidden), kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(1), wt, T, units, c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
   } else {
     const int d = c.d_shared;
     const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, false, ntt, 4, t0, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, t0, kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, true, ntt, 4, tiles_bound(act_exps, d), kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, 4, tiles_bound(act_exps, d),
+                                   kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(2), wt, 1, false, ntt, 4, tiles_bound(act_exps, d), kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(2), wt, 1, GEMM_PLAIN, ntt, 4, tiles_bound(act_exps, d),
+                                   kGridCap, s));
     DEAMOE_TRY(ev.mark());
     ZsumArgs za;
     za.counts = pc;
@@ -351,8 +368,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     za.act_f32 = c.act_dtype == DEAMOE_F32;
     DEAMOE_TRY(launch_zsum(za, T * dk, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(3), wt, 1, false, ntt, DEAMOE_KS_DOWN,
-                                   tiles_bound(act_depts + se, c.hidden), kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(3), wt, T, act_depts + se, c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
   }
   CombineArgs ca;

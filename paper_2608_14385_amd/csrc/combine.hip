@@ -6,8 +6,11 @@
 namespace deamoe {
 
 // y[t, c] = sum over the token's slots, in slot order, of w * partial[pair, c];
-// rounded once to the output type.  One thread per 4 consecutive columns.
-__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
+// rounded once to the output type.  One thread per 4 consecutive columns;
+// the slots are taken in batches whose loads are all issued before the
+// batch is summed (selects, not branches, so that they are not serialized).
+__global__ __launch_bounds__(64) void combine_kernel(CombineArgs a) {
+  constexpr int U = 8;
   const int t = blockIdx.y;
   const int c = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (c >= a.h) return;
@@ -15,9 +18,20 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   const int32_t *sp = a.slot_pair + (size_t)t * a.max_slots;
   const float *sw = a.slot_w + (size_t)t * a.max_slots;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < ns; ++s) {
-    const f32x4 v = *reinterpret_cast<const f32x4 *>(a.partial + (size_t)sp[s] * a.h + c);
-    acc += sw[s] * v;
+  for (int s0 = 0; s0 < ns; s0 += U) {
+    f32x4 v[U];
+    float w[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = min(s0 + u, ns - 1);
+      w[u] = sw[s];
+      v[u] = *reinterpret_cast<const f32x4 *>(a.partial + (size_t)sp[s] * a.h + c);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const f32x4 nx = acc + w[u] * v[u];
+      acc = s0 + u < ns ? nx : acc;
+    }
   }
   if (a.act_f32) {
     *reinterpret_cast<f32x4 *>(static_cast<float *>(a.y) + (size_t)t * a.h + c) = acc;
@@ -29,8 +43,8 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
 }
 
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s) {
-  dim3 grid((a.h / 4 + 255) / 256, a.T);
-  hipLaunchKernelGGL(combine_kernel, grid, dim3(256), 0, s, a);
+  dim3 grid((a.h / 4 + 63) / 64, a.T);
+  hipLaunchKernelGGL(combine_kernel, grid, dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

@@ -9,9 +9,9 @@ namespace deamoe {
 
 constexpr int kMaxUnitsCached = 4096;
 
-template <int WT, int NW, int NTT, int KS, bool SPLIT>
+template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR>
 __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
-  using Run = TileRunner<WT, NW, NTT, KS, SPLIT>;
+  using Run = TileRunner<WT, NW, NTT, KS, SPLIT, PAIR>;
   __shared__ typename Run::Smem sm;
   __shared__ int32_t s_begin[kMaxUnitsCached];
   const int n_units = st.counts[0], n_tiles = st.counts[1];
@@ -36,56 +36,67 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
   }
 }
 
+// mode: GemmMode; row pairs exist for NTT <= 2 only (the host picks them so)
 template <int WT, int NW, int NTT, int KS>
-static hipError_t launch_gemm(const GemmStage &st, bool split, int max_tiles, int grid_cap,
+static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int grid_cap,
                               hipStream_t s) {
   constexpr int TPB = 4 / KS;
   int grid = (max_tiles + TPB - 1) / TPB;
   grid = grid < 1 ? 1 : (grid > grid_cap ? grid_cap : grid);
   if constexpr (NW == 2) {
-    if (split) {
-      hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, true>), dim3(grid), dim3(256), 0, s, st);
+    if (mode == 1) {
+      hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, true, false>), dim3(grid), dim3(256),
+                         0, s, st);
       return hipGetLastError();
     }
+    if (mode == 2) {
+      if constexpr (NTT <= 2) {   // row pairs are built for up to two token tiles
+        hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false, true>), dim3(grid),
+                           dim3(256), 0, s, st);
+        return hipGetLastError();
+      }
+      return hipErrorInvalidValue;
+    }
   }
-  hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false>), dim3(grid), dim3(256), 0, s, st);
+  hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false, false>), dim3(grid), dim3(256), 0,
+                     s, st);
   return hipGetLastError();
 }
 
 template <int WT, int NW, int KS>
-static hipError_t dispatch_ntt(const GemmStage &st, bool split, int ntt, int max_tiles, int cap,
+static hipError_t dispatch_ntt(const GemmStage &st, int mode, int ntt, int max_tiles, int cap,
                                hipStream_t s) {
   switch (ntt) {
-    case 1: return launch_gemm<WT, NW, 1, KS>(st, split, max_tiles, cap, s);
-    case 2: return launch_gemm<WT, NW, 2, KS>(st, split, max_tiles, cap, s);
-    case 4: return launch_gemm<WT, NW, 4, KS>(st, split, max_tiles, cap, s);
-    default: return launch_gemm<WT, NW, 8, KS>(st, split, max_tiles, cap, s);
+    case 1: return launch_gemm<WT, NW, 1, KS>(st, mode, max_tiles, cap, s);
+    case 2: return launch_gemm<WT, NW, 2, KS>(st, mode, max_tiles, cap, s);
+    case 4: return launch_gemm<WT, NW, 4, KS>(st, mode, max_tiles, cap, s);
+    default: return launch_gemm<WT, NW, 8, KS>(st, mode, max_tiles, cap, s);
   }
 }
 
 template <int WT, int NW>
-static hipError_t dispatch_ks(const GemmStage &st, bool split, int ntt, int ks, int max_tiles,
+static hipError_t dispatch_ks(const GemmStage &st, int mode, int ntt, int ks, int max_tiles,
                               int cap, hipStream_t s) {
   switch (ks) {
-    case 1: return dispatch_ntt<WT, NW, 1>(st, split, ntt, max_tiles, cap, s);
-    case 2: return dispatch_ntt<WT, NW, 2>(st, split, ntt, max_tiles, cap, s);
-    default: return dispatch_ntt<WT, NW, 4>(st, split, ntt, max_tiles, cap, s);
+    case 1: return dispatch_ntt<WT, NW, 1>(st, mode, ntt, max_tiles, cap, s);
+    case 2: return dispatch_ntt<WT, NW, 2>(st, mode, ntt, max_tiles, cap, s);
+    default: return dispatch_ntt<WT, NW, 4>(st, mode, ntt, max_tiles, cap, s);
   }
 }
 
-hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, bool split, int ntt,
+hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int mode, int ntt,
                                int ks, int max_tiles, int grid_cap, hipStream_t s) {
   if (nw == 2) {
     switch (wtype) {
-      case WT_F32: return dispatch_ks<WT_F32, 2>(st, split, ntt, ks, max_tiles, grid_cap, s);
-      case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, split, ntt, ks, max_tiles, grid_cap, s);
-      default: return dispatch_ks<WT_FP8, 2>(st, split, ntt, ks, max_tiles, grid_cap, s);
+      case WT_F32: return dispatch_ks<WT_F32, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
+      case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
+      default: return dispatch_ks<WT_FP8, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
     }
   }
   switch (wtype) {
-    case WT_F32: return dispatch_ks<WT_F32, 1>(st, false, ntt, ks, max_tiles, grid_cap, s);
-    case WT_BF16: return dispatch_ks<WT_BF16, 1>(st, false, ntt, ks, max_tiles, grid_cap, s);
-    default: return dispatch_ks<WT_FP8, 1>(st, false, ntt, ks, max_tiles, grid_cap, s);
+    case WT_F32: return dispatch_ks<WT_F32, 1>(st, 0, ntt, ks, max_tiles, grid_cap, s);
+    case WT_BF16: return dispatch_ks<WT_BF16, 1>(st, 0, ntt, ks, max_tiles, grid_cap, s);
+    default: return dispatch_ks<WT_FP8, 1>(st, 0, ntt, ks, max_tiles, grid_cap, s);
   }
 }
 

@@ -142,7 +142,9 @@ __device__ inline void step_mma(const u32x4 (&a)[NW][4], const u32x4 (&B)[NTT][S
 }
 
 // Stream one work item: row tiles rt0 .. rt0 + nsub - 1 of unit U, each over
-// the K steps kp, kp + ks, ... (nsub > 1 only when ks == 1).  `lds` is this
+// the K steps kp, kp + ks, ... (nsub > 1 only when ks == 1).  PAIR: a tile is
+// 32 rows of one matrix, streamed as two 16-row halves (w0 and w0 + 16 rows)
+// that share the token operand; R is then a multiple of 32.  `lds` is this
 // wave's private staging region (NW * WLoad<WT>::REGION bytes).
 // Rows past R and tokens past ntok are clamped to valid ones: their products
 // land only in output rows / columns that are never stored.
@@ -153,9 +155,11 @@ __device__ inline void step_mma(const u32x4 (&a)[NW][4], const u32x4 (&B)[NTT][S
 // row instead of weights, so every iteration issues the same loads.
 // `done(rt, acc)` is called (and acc cleared) after the last K step of
 // each tile when nsub > 1; with nsub == 1 the caller finishes the tile.
-template <int WT, int NW, int NTT, bool SPLIT, int PF, class Done>
+template <int WT, int NW, int NTT, bool SPLIT, int PF, bool PAIR, class Done>
 __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, int ks,
                                  char *lds, f32x4 (&acc)[NW][NTT], Done done) {
+  static_assert(!PAIR || (NW == 2 && !SPLIT), "a row pair is two tiles of one matrix");
+  constexpr int TR = PAIR ? 2 * kTile : kTile;   // weight rows of a tile
   using Tr = WTraits<WT>;
   using LD = WLoad<WT>;
   constexpr int NB = PF + 1;
@@ -181,7 +185,9 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
   // load pattern: instruction q covers rows q * RPI + lane / LPR, 16 bytes each
   const int lrow = lane / LD::LPR, lchunk = lane % LD::LPR;
   const char *w0 = static_cast<const char *>(U.w0) + lchunk * 16;
-  const char *w1 = NW == 2 ? static_cast<const char *>(U.w1) + lchunk * 16 : w0;
+  const char *w1 = PAIR ? w0 + (size_t)kTile * ldw * Tr::W_BYTES
+                        : NW == 2 ? static_cast<const char *>(U.w1) + lchunk * 16 : w0;
+  const int rmax = R - 1 - (PAIR ? kTile : 0);   // last row the first matrix may read
   const char *dummy = bp0[0] + (lane & 15) * 16;
   const int sblocks = U.K / 128;
   u32x4 G[NB][NW][LD::NQ];
@@ -194,7 +200,7 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
     const int kstep = ok ? kp + (v - sub * nloc) * ks : 0;
 #pragma unroll
     for (int q = 0; q < LD::NQ; ++q) {
-      const int row = min((rt0 + sub) * kTile + q * LD::RPI + lrow, R - 1);
+      const int row = min((rt0 + sub) * TR + q * LD::RPI + lrow, rmax);
       const size_t woff = (size_t)row * ldw * Tr::W_BYTES + (size_t)kstep * LD::WSEG;
 #pragma unroll
       for (int n = 0; n < NW; ++n)
@@ -202,9 +208,9 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
     }
     load_b<WT, NTT, SPLIT>(Bb, bp0, bp1, ntt, (size_t)kstep * ASEG, g);
     if constexpr (WT == WT_FP8) {
-      const int srow = ((rt0 + sub) * kTile) / 128;
+      const int srow = ((rt0 + sub) * TR) / 128;   // a row pair lies in one scale block
       sc[0] = U.s0[srow * sblocks + kstep];
-      if constexpr (NW == 2) sc[1] = U.s1[srow * sblocks + kstep];
+      if constexpr (NW == 2) sc[1] = (PAIR ? U.s0 : U.s1)[srow * sblocks + kstep];
     }
   };
   // rows of the staged step in the matrix-core operand layout
@@ -287,14 +293,16 @@ __device__ inline f32x4 sigma4(f32x4 v, int sigma) {
 }
 
 // Write the finished tile.  Lane l holds rows 4 * (l / 16) + r, r < 4, of
-// the tile for token (l % 16) of each token tile.
-template <int NW, int NTT>
+// the tile for token (l % 16) of each token tile.  PAIR: the second
+// accumulator holds the 16 rows after the first (same epilogue, one matrix).
+template <int NW, int NTT, bool PAIR>
 __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int sigma, const f32x4 (&acc)[NW][NTT]) {
+  constexpr int TR = PAIR ? 2 * kTile : kTile;
   const int lane = lane_id();
   const int g = lane >> 4, j = lane & 15;
   const int R = uniform(U.R), ntok = uniform(U.ntok), epi = uniform(U.epi);
   const int out_f32 = uniform(U.out_f32), ldout = uniform(U.ldout);
-  const int row0 = rt * kTile + 4 * g;
+  const int row0 = rt * TR + 4 * g;
   if (row0 >= R) return;
   const bool full = row0 + 3 < R;
   const int ntt = uniform(min(NTT, (ntok + kTile - 1) / kTile));
@@ -305,7 +313,14 @@ __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int sigma, const
     if (i >= ntok) continue;
     const size_t off = (size_t)i * ldout + row0;
     const f32x4 v0 = acc[0][tt];
-    if constexpr (NW == 2) {
+    if constexpr (PAIR) {
+      const f32x4 v1 = acc[1][tt];
+      const int row1 = row0 + kTile;
+      store4(U.out0, out_f32, off, epi == EPI_SIGMA ? sigma4(v0, sigma) : v0, full, R - row0);
+      if (row1 < R)
+        store4(U.out0, out_f32, off + kTile, epi == EPI_SIGMA ? sigma4(v1, sigma) : v1,
+               row1 + 3 < R, R - row1);
+    } else if constexpr (NW == 2) {
       const f32x4 v1 = acc[1][tt];
       if (epi == EPI_SWIGLU) {
         const f32x4 o = f32x4{silu_f(v0[0]) * v1[0], silu_f(v0[1]) * v1[1], silu_f(v0[2]) * v1[2],
@@ -333,8 +348,9 @@ __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int sigma, const
 #ifndef DEAMOE_PF_NW2
 #define DEAMOE_PF_NW2 1
 #endif
-template <int WT, int NW, int NTT, int KS, bool SPLIT = false>
+template <int WT, int NW, int NTT, int KS, bool SPLIT = false, bool PAIR = false>
 struct TileRunner {
+  static constexpr int TR = PAIR ? 2 * kTile : kTile;   // weight rows of a tile
   static constexpr int TPB = 4 / KS;
   // load groups in flight per wave
   static constexpr int PF = NTT > 2 ? 1 : (NW == 1 ? DEAMOE_PF_NW1 : DEAMOE_PF_NW2);
@@ -357,11 +373,13 @@ struct TileRunner {
     int rt0 = 0, nsub = 1;
     if (active) {
       const int tpg = KS == 1 ? uniform(U->tpg) : 1;
-      const int ntiles = (uniform(U->R) + kTile - 1) / kTile;
+      const int ntiles = (uniform(U->R) + TR - 1) / TR;
       rt0 = item * tpg;
       nsub = min(tpg, ntiles - rt0);
-      auto done = [&](int rt, const f32x4 (&a)[NW][NTT]) { tile_epilogue<NW, NTT>(*U, rt, sigma, a); };
-      tile_loop<WT, NW, NTT, SPLIT, PF>(*U, rt0, nsub, kp, KS, sm.buf[wave], acc, done);
+      auto done = [&](int rt, const f32x4 (&a)[NW][NTT]) {
+        tile_epilogue<NW, NTT, PAIR>(*U, rt, sigma, a);
+      };
+      tile_loop<WT, NW, NTT, SPLIT, PF, PAIR>(*U, rt0, nsub, kp, KS, sm.buf[wave], acc, done);
     }
     if constexpr (KS > 1) {
       f32x4 *red = reinterpret_cast<f32x4 *>(sm.buf[wave]);
@@ -383,7 +401,7 @@ struct TileRunner {
       }
       __syncthreads();
     }
-    if (active && kp == 0 && nsub == 1) tile_epilogue<NW, NTT>(*U, rt0, sigma, acc);
+    if (active && kp == 0 && nsub == 1) tile_epilogue<NW, NTT, PAIR>(*U, rt0, sigma, acc);
   }
 };
 

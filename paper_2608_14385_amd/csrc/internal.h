@@ -19,6 +19,13 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define DEAMOE_KS_DOWN 1
 #endif
 
+// Down-projection stages stream two adjacent 16-row tiles of a matrix per
+// wave (one token operand for both) for up to 32 tokens; 0 always streams
+// single tiles.
+#ifndef DEAMOE_DOWN_PAIR
+#define DEAMOE_DOWN_PAIR 1
+#endif
+
 constexpr int kWave = 64;
 constexpr int kTile = 16;   // MFMA tile edge: 16 weight rows x 16 tokens
 

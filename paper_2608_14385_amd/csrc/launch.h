@@ -37,6 +37,7 @@ struct RouteArgs {
   int32_t T, n, m, k, kdept, E, score, renorm;
   float route_scale;
   int32_t h, d_s, d_p, d_se, act_f32, w_bytes, fp8, plan;
+  int32_t down_rows;     // weight rows of a down-projection tile (16, or 32 for row pairs)
   // logits: sum of kc partial products, or injected; optional bias
   const float *part;
   int32_t kc, ldp;
@@ -77,8 +78,15 @@ struct ZsumArgs {
 hipError_t launch_router(const RouterArgs &a, int wtype, int ntt, int kc, hipStream_t s);
 // The per-token kernel (grid T) followed by the plan kernel (one workgroup).
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
-// split: the stage's two matrices read different token operands (in0 / in1).
-hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, bool split, int ntt,
+// Token-operand modes of two-matrix stages (nw == 2).
+enum GemmMode : int {
+  GEMM_PLAIN = 0,   // both matrices read the same token operand
+  GEMM_SPLIT = 1,   // the two matrices read different token operands (in0 / in1)
+  GEMM_PAIR = 2,    // the "two matrices" are adjacent 16-row tiles of one matrix
+};
+// max_tiles bounds the stage's work items (row tiles of kTile rows, or of
+// 2 * kTile rows in GEMM_PAIR mode) for the grid size.
+hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int mode, int ntt,
                                int ks, int max_tiles, int grid_cap, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 hipError_t launch_zsum(const ZsumArgs &a, int max_dept_pairs, hipStream_t s);

@@ -188,10 +188,12 @@ __device__ inline void put_unit(GemmUnit *U, const void *w0, const void *w1, con
 
 // Row tiles per work item of a stage whose K is not split across waves: short
 // contractions take several tiles so that a work item streams enough bytes.
-__device__ inline int tiles_per_item(int K) {
-  return DEAMOE_KS_DOWN > 1 ? 1 : max(1, min(8, 2048 / K));
+__device__ inline int tiles_per_item(int K, int rows) {
+  return DEAMOE_KS_DOWN > 1 ? 1 : max(1, min(8, 2048 * kTile / (rows * K)));
 }
-__device__ inline int items_of(int R, int tpg) { return ((R + kTile - 1) / kTile + tpg - 1) / tpg; }
+__device__ inline int items_of(int R, int tpg, int rows) {
+  return ((R + rows - 1) / rows + tpg - 1) / tpg;
+}
 
 __device__ inline bool bit_at(const uint32_t *row, int i) { return (row[i >> 5] >> (i & 31)) & 1; }
 
@@ -228,22 +230,27 @@ __device__ inline void load_run(const float *p, float (&v)[NS]) {
 
 __device__ inline int popc64(uint64_t v) { return __popcll(v); }
 
-// One wave per token (grid = T): logits, optional group limit, top-k,
-// routing weights and the token's distinct departments with P_{t,j}; the
-// token's combine slots when a plan follows.
+// One wave routes one token: logits, optional group limit, top-k, routing
+// weights and the token's distinct departments with P_{t,j}; the token's
+// combine slots when a plan follows.
 //
 // Top-k works on order keys (a monotone map of the logit to an unsigned
 // int).  A threshold is found by radix selection (built bit by bit from the
 // top; a bit stays if at least k keys reach the value), first over the
 // per-lane maxima; the few candidates at or above it rank themselves by
 // (logit desc, id asc) through LDS.
+struct TokSmem {
+  uint64_t sel[64];                  // candidates in expert order
+  uint64_t ord[kMaxK];               // winners in rank order
+  int32_t gs[kMaxMGrouped];          // department scores (group limit)
+  uint32_t db[kDW];                  // the token's department bitmap
+};
+
 template <int NS>
-__global__ __launch_bounds__(64) void route_token_kernel(RouteArgs a) {
-  __shared__ uint64_t s_sel[64];                // candidates in expert order
-  __shared__ uint64_t s_ord[kMaxK];             // winners in rank order
-  __shared__ int32_t s_gs[kMaxMGrouped];        // department scores (group limit)
-  __shared__ uint32_t s_db[kDW];                // the token's department bitmap
-  const int t = blockIdx.x, lane = threadIdx.x;
+__device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSmem &sm) {
+  uint64_t *s_sel = sm.sel, *s_ord = sm.ord;
+  int32_t *s_gs = sm.gs;
+  uint32_t *s_db = sm.db;
   const int n = a.n, k = a.k, E = a.E, m = a.m;
   const int dwords = (m + 31) / 32;
   const int e0 = lane * NS;
@@ -457,6 +464,12 @@ __global__ __launch_bounds__(64) void route_token_kernel(RouteArgs a) {
   }
 }
 
+template <int NS>
+__global__ __launch_bounds__(64) void route_token_kernel(RouteArgs a) {
+  __shared__ TokSmem sm;
+  route_one<NS>(a, blockIdx.x, threadIdx.x, sm);
+}
+
 // One workgroup: the per-department and per-expert token lists (ascending
 // token order) from the per-token results, then the unit tables of every
 // expert stage and the combine slots.
@@ -467,17 +480,22 @@ __global__ __launch_bounds__(64) void route_token_kernel(RouteArgs a) {
 // placed independently.  Counts and the number of active units are summed
 // in one scan over departments then experts, packed as count | active << 16
 // (both sums stay below 2^16).
-template <int BT>
-__global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
-  constexpr int EPT = kMaxN / BT;   // experts per thread in the per-expert loops
-  __shared__ int32_t s_ids[kMaxTK];            // [t][rank] selected expert
-  __shared__ int32_t s_dep[kMaxTK];            // [t][slot] departments, -1 padded
-  __shared__ uint32_t s_etok[kMaxN * kTW];     // [e] token bitmap
-  __shared__ uint32_t s_dtok[kMaxM * kTW];     // [j] token bitmap
-  __shared__ int32_t s_scan[kMaxM + kMaxN];    // [depts, experts] packed prefix
-  __shared__ int32_t s_nd[kMaxT];
-  __shared__ int32_t s_tmp[64];
+struct PlanSmem {
+  int32_t ids[kMaxTK];               // [t][rank] selected expert
+  int32_t dep[kMaxTK];               // [t][slot] departments, -1 padded
+  uint32_t etok[kMaxN * kTW];        // [e] token bitmap
+  uint32_t dtok[kMaxM * kTW];        // [j] token bitmap
+  int32_t scan[kMaxM + kMaxN];       // [depts, experts] packed prefix
+  int32_t nd[kMaxT];
+  int32_t tmp[64];
+};
 
+// Every thread of the workgroup (BT threads) calls it.
+template <int BT>
+__device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
+  constexpr int EPT = kMaxN / BT;   // experts per thread in the per-expert loops
+  int32_t *s_ids = sm.ids, *s_dep = sm.dep, *s_scan = sm.scan, *s_nd = sm.nd, *s_tmp = sm.tmp;
+  uint32_t *s_etok = sm.etok, *s_dtok = sm.dtok;
   const int tid = threadIdx.x;
   const int T = a.T, n = a.n, m = a.m, k = a.k, E = a.E;
   const int tw = (T + 31) / 32;
@@ -573,9 +591,11 @@ __global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
   const deamoe_weights &W = a.w;
   if (slice) {
     const int ta_d = (a.d_s + kTile - 1) / kTile, ta_p = (a.d_p + kTile - 1) / kTile;
-    const int gd = tiles_per_item(a.d_s), gp = a.d_p ? tiles_per_item(a.d_p) : 1;
-    const int gse = a.d_se ? tiles_per_item(a.d_se) : 1;
-    const int bd = items_of(a.h, gd), bp = items_of(a.h, gp), bse = items_of(a.h, gse);
+    const int dr = a.down_rows;
+    const int gd = tiles_per_item(a.d_s, dr), gp = a.d_p ? tiles_per_item(a.d_p, dr) : 1;
+    const int gse = a.d_se ? tiles_per_item(a.d_se, dr) : 1;
+    const int bd = items_of(a.h, gd, dr), bp = items_of(a.h, gp, dr);
+    const int bse = items_of(a.h, gse, dr);
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_scan[j] >> 16, off = doff(j);
       const int32_t *idx = a.r.dept_tokens + off;
@@ -623,8 +643,9 @@ __global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
     }
   } else {  // PLAN_FACTORED
     const int d = a.d_s, td = (d + kTile - 1) / kTile;
-    const int gd = tiles_per_item(d), gse = a.d_se ? tiles_per_item(a.d_se) : 1;
-    const int bd = items_of(a.h, gd), bse = items_of(a.h, gse);
+    const int dr = a.down_rows;
+    const int gd = tiles_per_item(d, dr), gse = a.d_se ? tiles_per_item(a.d_se, dr) : 1;
+    const int bd = items_of(a.h, gd, dr), bse = items_of(a.h, gse, dr);
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_scan[j] >> 16, off = doff(j);
       const int32_t *idx = a.r.dept_tokens + off;
@@ -680,6 +701,12 @@ __global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
     a.counts->n_exp_pairs = nep_priv;
     a.counts->n_pairs = ndp + (slice ? nep_priv : 0) + (has_se ? T : 0);
   }
+}
+
+template <int BT>
+__global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
+  __shared__ PlanSmem sm;
+  plan_body<BT>(a, sm);
 }
 
 hipError_t launch_route(const RouteArgs &a, hipStream_t s) {

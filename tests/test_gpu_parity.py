@@ -161,14 +161,15 @@ def test_deterministic_and_route_only():
         assert np.array_equal(h1[k], h3[k]), k
 
 
+@pytest.mark.parametrize("T", [12, 40])
 @pytest.mark.parametrize("preset", ["tiny_f32", "7b_bf16", "dsv3_bf16", "dsv3_factored"])
-def test_route_ties(preset):
+def test_route_ties(preset, T):
     """Coarse injected logits: many exact ties, including every logit equal
     (more candidates than one per lane, so the exact selection path runs) and
     a few equal values at the top (the candidate path); the lower id wins."""
     cfg = P[preset].layer
-    T, n = 12, cfg.n_experts
-    g = torch.Generator(device="cpu").manual_seed(5)
+    n = cfg.n_experts
+    g = torch.Generator(device="cpu").manual_seed(5 + T)
     u = torch.rand(T, n, generator=g)
     rows = [torch.full((n,), 0.5),                                  # all equal
             torch.round(u[1] * 4) / 4,                              # five levels
