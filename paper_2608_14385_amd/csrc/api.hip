@@ -42,7 +42,7 @@ bool has_private(const deamoe_config &c) {
 struct Layout {
   size_t logits, part, topk_ids, topk_w, tok_depts, tok_dept_w, tok_ndept, dept_count,
       dept_offset, dept_tokens, exp_count, exp_offset, exp_tokens;
-  size_t counts, units[kMaxStages], slot_pair, slot_w, nslot, tok_exp_pair, exp_src;
+  size_t counts, units[kMaxStages], slot_pair, slot_w, nslot, tok_exp_pair, exp_src, pair_dept;
   size_t abuf_dept, abuf_exp, abuf_se, gbuf, ubuf, ybuf, zbuf, zsbuf, partial;
   size_t total;
   int kc, max_units, max_dept_pairs, max_exp_pairs;
@@ -84,6 +84,7 @@ Layout make_layout(const deamoe_config &c) {
   L.nslot = take(T * 4);
   L.tok_exp_pair = take(T * k * 4);
   L.exp_src = take(T * k * 4);
+  L.pair_dept = take((size_t)L.max_dept_pairs * 4);
   const size_t dpairs = L.max_dept_pairs, epairs = L.max_exp_pairs;
   const size_t ds = c.d_shared, dp = c.d_private, dse = c.d_shared_expert;
   L.abuf_se = take(T * dse * ab);
@@ -160,6 +161,16 @@ int ntt_of(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
 // enough for both halves' accumulators to stay in registers.
 int down_rows_of(int T) { return DEAMOE_DOWN_PAIR && ntt_of(T) <= 2 ? 2 * kTile : kTile; }
 
+// Waves sharing one down-projection tile.  The SLICE form packs several
+// short private tiles per work item and keeps whole tiles per wave; the
+// FACTORED form (every contraction d long) splits K while the batch leaves
+// too few tiles to occupy the waves.
+int down_ks_of(const deamoe_config &c, int T) {
+  if (c.form == DEAMOE_FORM_SLICE) return DEAMOE_KS_DOWN;
+  return T <= DEAMOE_FDOWN_KS4_T ? 4 : T <= DEAMOE_FDOWN_KS2_T ? 2 : 1;
+}
+
+
 template <class P>
 P *at(void *ws, size_t off) {
   return reinterpret_cast<P *>(static_cast<char *>(ws) + off);
@@ -223,6 +234,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.fp8 = c.w_dtype == DEAMOE_FP8_E4M3_B128;
   a.plan = plan;
   a.down_rows = down_rows_of(T);
+  a.down_ks = down_ks_of(c, T);
   a.part = at<float>(ws, L.part);
   a.kc = L.kc;
   a.ldp = 64 * route_ns(c.n_experts);
@@ -236,6 +248,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.slot_w = at<float>(ws, L.slot_w);
   a.tok_exp_pair = at<int32_t>(ws, L.tok_exp_pair);
   a.exp_src = at<int32_t>(ws, L.exp_src);
+  a.pair_dept = at<int32_t>(ws, L.pair_dept);
   a.max_slots = max_slots_of(c);
   if (w) a.w = *w;
   a.x = x;
@@ -285,13 +298,13 @@ int tiles_bound(int units_max, int R, int rows = kTile) {
   return units_max * ((R + rows - 1) / rows);
 }
 
-// Launch of a down-projection stage (K split DEAMOE_KS_DOWN).
-hipError_t launch_down(const GemmStage &st, int wt, int T, int units_max, int R, int cap,
+// Launch of a down-projection stage.
+hipError_t launch_down(const GemmStage &st, int wt, int T, int ks, int units_max, int R, int cap,
                        hipStream_t s) {
   const int rows = down_rows_of(T);
   const bool pair = rows == 2 * kTile;
-  return launch_grouped_gemm(st, wt, pair ? 2 : 1, pair ? GEMM_PAIR : GEMM_PLAIN, ntt_of(T),
-                             DEAMOE_KS_DOWN, tiles_bound(units_max, R, rows), cap, s);
+  return launch_grouped_gemm(st, wt, pair ? 2 : 1, pair ? GEMM_PAIR : GEMM_PLAIN, ntt_of(T), ks,
+                             tiles_bound(units_max, R, rows), cap, s);
 }
 
 constexpr int kGridCap = 8192;   // 256 CUs x 32 workgroups
@@ -339,23 +352,22 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, ta, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
-    DEAMOE_TRY(launch_down(stage(1), wt, T, units, c.hidden, kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(1), wt, T, down_ks_of(c, T), units, c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
   } else {
     const int d = c.d_shared;
     const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
     DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, t0, kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, 4, tiles_bound(act_exps, d),
-                                   kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, DEAMOE_KS_FPRIV,
+                                   tiles_bound(act_exps, d), kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(2), wt, 1, GEMM_PLAIN, ntt, 4, tiles_bound(act_exps, d),
-                                   kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(2), wt, T, down_ks_of(c, T), act_exps, d, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     ZsumArgs za;
     za.counts = pc;
     za.dept_tokens = r.dept_tokens;
-    za.dept_offset = r.dept_offset;
+    za.pair_dept = at<int32_t>(ws, L.pair_dept);
     za.topk_ids = r.topk_ids;
     za.tok_exp_pair = at<int32_t>(ws, L.tok_exp_pair);
     za.topk_w = r.topk_w;
@@ -368,7 +380,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     za.act_f32 = c.act_dtype == DEAMOE_F32;
     DEAMOE_TRY(launch_zsum(za, T * dk, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_down(stage(3), wt, T, act_depts + se, c.hidden, kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(3), wt, T, down_ks_of(c, T), act_depts + se, c.hidden, kGridCap,
+                           s));
     DEAMOE_TRY(ev.mark());
   }
   CombineArgs ca;

@@ -26,6 +26,19 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define DEAMOE_DOWN_PAIR 1
 #endif
 
+// K split of the FACTORED private gate/up stage (A_g G, A_u U).
+#ifndef DEAMOE_KS_FPRIV
+#define DEAMOE_KS_FPRIV 2
+#endif
+// FACTORED down-projection stages split K four ways up to this many tokens,
+// two ways up to the next.
+#ifndef DEAMOE_FDOWN_KS4_T
+#define DEAMOE_FDOWN_KS4_T 8
+#endif
+#ifndef DEAMOE_FDOWN_KS2_T
+#define DEAMOE_FDOWN_KS2_T 16
+#endif
+
 constexpr int kWave = 64;
 constexpr int kTile = 16;   // MFMA tile edge: 16 weight rows x 16 tokens
 

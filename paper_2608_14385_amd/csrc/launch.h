@@ -38,6 +38,7 @@ struct RouteArgs {
   float route_scale;
   int32_t h, d_s, d_p, d_se, act_f32, w_bytes, fp8, plan;
   int32_t down_rows;     // weight rows of a down-projection tile (16, or 32 for row pairs)
+  int32_t down_ks;       // waves sharing one down-projection tile (K split)
   // logits: sum of kc partial products, or injected; optional bias
   const float *part;
   int32_t kc, ldp;
@@ -48,6 +49,7 @@ struct RouteArgs {
   PlanCounts *counts;
   GemmUnit *units[kMaxStages];
   int32_t *slot_pair, *nslot, *tok_exp_pair, *exp_src;
+  int32_t *pair_dept;    // FACTORED: department of every department pair
   float *slot_w;
   int32_t max_slots;
   // inputs of the planned stages
@@ -69,7 +71,7 @@ struct CombineArgs {
 
 struct ZsumArgs {
   const PlanCounts *counts;
-  const int32_t *dept_tokens, *dept_offset, *topk_ids, *tok_exp_pair;
+  const int32_t *dept_tokens, *pair_dept, *topk_ids, *tok_exp_pair;
   const float *topk_w, *z;
   void *zs;
   int32_t m, k, E, d, act_f32;

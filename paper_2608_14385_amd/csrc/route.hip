@@ -188,8 +188,8 @@ __device__ inline void put_unit(GemmUnit *U, const void *w0, const void *w1, con
 
 // Row tiles per work item of a stage whose K is not split across waves: short
 // contractions take several tiles so that a work item streams enough bytes.
-__device__ inline int tiles_per_item(int K, int rows) {
-  return DEAMOE_KS_DOWN > 1 ? 1 : max(1, min(8, 2048 * kTile / (rows * K)));
+__device__ inline int tiles_per_item(int K, int rows, int ks) {
+  return ks > 1 ? 1 : max(1, min(8, 2048 * kTile / (rows * K)));
 }
 __device__ inline int items_of(int R, int tpg, int rows) {
   return ((R + rows - 1) / rows + tpg - 1) / tpg;
@@ -570,6 +570,7 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       const int pd = doff(j) + rank_below(s_dtok + j * kTW, t);
       a.r.dept_tokens[pd] = t;
       if (a.plan) a.slot_pair[(size_t)t * S + q] = pd;
+      if (a.plan == PLAN_FACTORED) a.pair_dept[pd] = j;
     }
   }
   if (!a.plan) return;
@@ -591,9 +592,9 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
   const deamoe_weights &W = a.w;
   if (slice) {
     const int ta_d = (a.d_s + kTile - 1) / kTile, ta_p = (a.d_p + kTile - 1) / kTile;
-    const int dr = a.down_rows;
-    const int gd = tiles_per_item(a.d_s, dr), gp = a.d_p ? tiles_per_item(a.d_p, dr) : 1;
-    const int gse = a.d_se ? tiles_per_item(a.d_se, dr) : 1;
+    const int dr = a.down_rows, dk = a.down_ks;
+    const int gd = tiles_per_item(a.d_s, dr, dk), gp = a.d_p ? tiles_per_item(a.d_p, dr, dk) : 1;
+    const int gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
     const int bd = items_of(a.h, gd, dr), bp = items_of(a.h, gp, dr);
     const int bse = items_of(a.h, gse, dr);
     if (tid < m && my_dc > 0) {
@@ -643,9 +644,11 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
     }
   } else {  // PLAN_FACTORED
     const int d = a.d_s, td = (d + kTile - 1) / kTile;
-    const int dr = a.down_rows;
-    const int gd = tiles_per_item(d, dr), gse = a.d_se ? tiles_per_item(a.d_se, dr) : 1;
+    const int dr = a.down_rows, dk = a.down_ks;
+    const int gd = tiles_per_item(d, dr, dk), gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
     const int bd = items_of(a.h, gd, dr), bse = items_of(a.h, gse, dr);
+    // A_d^T: d x d, streamed like the down projections
+    const int g2 = tiles_per_item(d, dr, dk), b2 = items_of(d, g2, dr);
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_scan[j] >> 16, off = doff(j);
       const int32_t *idx = a.r.dept_tokens + off;
@@ -671,7 +674,7 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
                a.act_f32);
       put_unit(&a.units[2][u], wptr(W.priv_down, e, d, d), nullptr, sptr(W.scale[5], e, d, d),
                nullptr, yo, yo, nullptr, a.zbuf + (size_t)off * d, nullptr, d, d, d, d,
-               my_ec[q], u * td, EPI_SIGMA, 1);
+               my_ec[q], u * b2, EPI_SIGMA, 1, g2);
     }
     if (tid == 0) {
       int units0 = ud, tiles0 = ud * td, units3 = ud;
@@ -691,7 +694,7 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       a.counts->stage[1][0] = ue;
       a.counts->stage[1][1] = ue * td;
       a.counts->stage[2][0] = ue;
-      a.counts->stage[2][1] = ue * td;
+      a.counts->stage[2][1] = ue * b2;
       a.counts->stage[3][0] = units3;
       a.counts->stage[3][1] = ud * bd + (has_se ? bse : 0);
     }
