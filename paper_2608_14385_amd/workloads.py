@@ -120,6 +120,18 @@ def _make_presets() -> dict:
                      renorm=True, sigma="silu", w_dtype="bf16", act_dtype="bf16")
     p["dsv3_factored"] = Workload(m6, _vanilla(m6, "dsv3_vanilla_256x2048", 256, 8, 2048),
                                   (1, 2, 4, 8, 16, 32, 64))
+    # The Qwen3-235B-A22B and Baseline-7B rows of Table 1 (Sec. 3.3), FACTORED
+    # form, each against its MoE baseline; softmax with renormalised top-k.
+    qw = LayerConfig("qwen3_factored", hidden=4096, n_experts=320, n_depts=8, top_k=8,
+                     top_k_dept=5, d_shared=1536, form="factored", score="softmax",
+                     renorm=True, sigma="silu", w_dtype="bf16", act_dtype="bf16")
+    p["qwen3_factored"] = Workload(qw, _vanilla(qw, "qwen3_vanilla_128x1536", 128, 8, 1536),
+                                   (1, 4, 16, 64))
+    b7 = LayerConfig("base7b_factored", hidden=1024, n_experts=672, n_depts=8, top_k=10,
+                     top_k_dept=4, d_shared=384, form="factored", score="softmax",
+                     renorm=True, sigma="silu", w_dtype="bf16", act_dtype="bf16")
+    p["base7b_factored"] = Workload(b7, _vanilla(b7, "base7b_vanilla_256x384", 256, 8, 384),
+                                    (1, 4, 16, 64))
     return p
 
 

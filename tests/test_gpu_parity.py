@@ -136,6 +136,15 @@ def test_dsv3_factored(T):
     check_case(case, tokens=sample_tokens(T, 2))
 
 
+@pytest.mark.parametrize("preset", ["qwen3_factored", "base7b_factored"])
+@pytest.mark.parametrize("T", [1, 16])
+def test_table1_factored(preset, T):
+    """The Qwen3-235B-A22B and Baseline-7B rows of Table 1 (FACTORED form,
+    group-limited top-k, softmax)."""
+    case = Case(P[preset].layer, T, seed=110 + T)
+    check_case(case, tokens=sample_tokens(T, 2))
+
+
 def test_dsv3_baseline():
     case = Case(P["dsv3_bf16"].baseline, 16, seed=90)
     check_case(case, tokens=sample_tokens(16, 2), baseline=True)
