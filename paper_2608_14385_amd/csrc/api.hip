@@ -157,9 +157,18 @@ int validate_weights(const deamoe_config &c, const deamoe_weights *w, bool need_
 
 int ntt_of(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
 
+// Token tiles per wave in the expert stages: at most 2, so that row pairs
+// and two-matrix tiles keep their accumulators in registers.  A unit with
+// more tokens than one wave holds gets one work item per token group.
+int wave_ntt_of(int T) { return T <= kTile ? 1 : 2; }
+int token_groups_max(int T) {
+  const int gt = kTile * wave_ntt_of(T);
+  return (T + gt - 1) / gt;
+}
+
 // Rows of a down-projection tile: row pairs while the token tiles are few
 // enough for both halves' accumulators to stay in registers.
-int down_rows_of(int T) { return DEAMOE_DOWN_PAIR && ntt_of(T) <= 2 ? 2 * kTile : kTile; }
+int down_rows_of(int) { return DEAMOE_DOWN_PAIR ? 2 * kTile : kTile; }
 
 // Waves sharing one down-projection tile.  The SLICE form packs several
 // short private tiles per work item and keeps whole tiles per wave; the
@@ -235,6 +244,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.plan = plan;
   a.down_rows = down_rows_of(T);
   a.down_ks = down_ks_of(c, T);
+  a.wave_tokens = kTile * wave_ntt_of(T);
   a.part = at<float>(ws, L.part);
   a.kc = L.kc;
   a.ldp = 64 * route_ns(c.n_experts);
@@ -303,8 +313,8 @@ hipError_t launch_down(const GemmStage &st, int wt, int T, int ks, int units_max
                        hipStream_t s) {
   const int rows = down_rows_of(T);
   const bool pair = rows == 2 * kTile;
-  return launch_grouped_gemm(st, wt, pair ? 2 : 1, pair ? GEMM_PAIR : GEMM_PLAIN, ntt_of(T), ks,
-                             tiles_bound(units_max, R, rows), cap, s);
+  return launch_grouped_gemm(st, wt, pair ? 2 : 1, pair ? GEMM_PAIR : GEMM_PLAIN, wave_ntt_of(T),
+                             ks, tiles_bound(units_max, R, rows) * token_groups_max(T), cap, s);
 }
 
 constexpr int kGridCap = 8192;   // 256 CUs x 32 workgroups
@@ -332,7 +342,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
                      slice ? PLAN_SLICE : PLAN_FACTORED, w, ev, s);
   if (rc) return rc;
   const int wt = c.w_dtype == DEAMOE_F32 ? WT_F32 : c.w_dtype == DEAMOE_BF16 ? WT_BF16 : WT_FP8;
-  const int ntt = ntt_of(T);
+  const int ntt = wave_ntt_of(T), groups = token_groups_max(T);
   const PlanCounts *pc = at<PlanCounts>(ws, L.counts);
   auto stage = [&](int i) {
     GemmStage st;
@@ -349,7 +359,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     const int ta = tiles_bound(act_depts, c.d_shared) +
                    (c.d_private ? tiles_bound(act_exps, c.d_private) : 0) +
                    se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, ta, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, ta * groups, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
     DEAMOE_TRY(launch_down(stage(1), wt, T, down_ks_of(c, T), units, c.hidden, kGridCap, s));
@@ -357,10 +367,10 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
   } else {
     const int d = c.d_shared;
     const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, t0, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, t0 * groups, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, DEAMOE_KS_FPRIV,
-                                   tiles_bound(act_exps, d), kGridCap, s));
+                                   tiles_bound(act_exps, d) * groups, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     DEAMOE_TRY(launch_down(stage(2), wt, T, down_ks_of(c, T), act_exps, d, kGridCap, s));
     DEAMOE_TRY(ev.mark());

@@ -63,14 +63,14 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
   return hipGetLastError();
 }
 
+// Token tiles per wave: 1 or 2 (larger token sets are split into groups).
 template <int WT, int NW, int KS>
 static hipError_t dispatch_ntt(const GemmStage &st, int mode, int ntt, int max_tiles, int cap,
                                hipStream_t s) {
   switch (ntt) {
     case 1: return launch_gemm<WT, NW, 1, KS>(st, mode, max_tiles, cap, s);
     case 2: return launch_gemm<WT, NW, 2, KS>(st, mode, max_tiles, cap, s);
-    case 4: return launch_gemm<WT, NW, 4, KS>(st, mode, max_tiles, cap, s);
-    default: return launch_gemm<WT, NW, 8, KS>(st, mode, max_tiles, cap, s);
+    default: return hipErrorInvalidValue;
   }
 }
 

@@ -156,7 +156,7 @@ __device__ inline void step_mma(const u32x4 (&a)[NW][4], const u32x4 (&B)[NTT][S
 // `done(rt, acc)` is called (and acc cleared) after the last K step of
 // each tile when nsub > 1; with nsub == 1 the caller finishes the tile.
 template <int WT, int NW, int NTT, bool SPLIT, int PF, bool PAIR, class Done>
-__device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, int ks,
+__device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, int ks, int tok0,
                                  char *lds, f32x4 (&acc)[NW][NTT], Done done) {
   static_assert(!PAIR || (NW == 2 && !SPLIT), "a row pair is two tiles of one matrix");
   constexpr int TR = PAIR ? 2 * kTile : kTile;   // weight rows of a tile
@@ -172,13 +172,14 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
   const int nloc = kp < nsteps ? (nsteps - kp + ks - 1) / ks : 0;   // K steps of this wave per tile
   const int total = nloc * nsub;
   if (total == 0) return;
-  const int ntt = uniform(min(NTT, (U.ntok + kTile - 1) / kTile));
+  const int ntok = uniform(U.ntok) - tok0;   // tokens of this item: tok0 .. U.ntok - 1
+  const int ntt = uniform(min(NTT, (ntok + kTile - 1) / kTile));
   const char *bp0[NTT];
   const char *bp1[NTT];
 #pragma unroll
   for (int tt = 0; tt < NTT; ++tt) {
     int i = tt * kTile + j;
-    i = i < U.ntok ? i : 0;
+    i = tok0 + (i < ntok ? i : 0);
     bp0[tt] = token_row(U.in0, U.idx, U.ldin, i, Tr::A_BYTES);
     bp1[tt] = SPLIT ? token_row(U.in1, U.idx, U.ldin, i, Tr::A_BYTES) : bp0[tt];
   }
@@ -296,11 +297,12 @@ __device__ inline f32x4 sigma4(f32x4 v, int sigma) {
 // the tile for token (l % 16) of each token tile.  PAIR: the second
 // accumulator holds the 16 rows after the first (same epilogue, one matrix).
 template <int NW, int NTT, bool PAIR>
-__device__ inline void tile_epilogue(const GemmUnit &U, int rt, int sigma, const f32x4 (&acc)[NW][NTT]) {
+__device__ inline void tile_epilogue(const GemmUnit &U, int rt, int tok0, int sigma,
+                                     const f32x4 (&acc)[NW][NTT]) {
   constexpr int TR = PAIR ? 2 * kTile : kTile;
   const int lane = lane_id();
   const int g = lane >> 4, j = lane & 15;
-  const int R = uniform(U.R), ntok = uniform(U.ntok), epi = uniform(U.epi);
+  const int R = uniform(U.R), ntok = uniform(U.ntok) - tok0, epi = uniform(U.epi);
   const int out_f32 = uniform(U.out_f32), ldout = uniform(U.ldout);
   const int row0 = rt * TR + 4 * g;
   if (row0 >= R) return;
@@ -311,7 +313,7 @@ __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int sigma, const
     if (tt > 0 && tt >= ntt) break;   // ntt >= 1
     const int i = tt * kTile + j;
     if (i >= ntok) continue;
-    const size_t off = (size_t)i * ldout + row0;
+    const size_t off = (size_t)(tok0 + i) * ldout + row0;
     const f32x4 v0 = acc[0][tt];
     if constexpr (PAIR) {
       const f32x4 v1 = acc[1][tt];
@@ -340,7 +342,9 @@ __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int sigma, const
 // One workgroup of 4 waves: 4 / KS work items, each split over KS waves
 // along K (interleaved K steps, partial tiles summed in a fixed order
 // through LDS; work items of one tile), or with KS == 1 one work item of
-// `tpg` tiles per wave.
+// `tpg` tiles per wave.  A unit with more than 16 * NTT tokens has one work
+// item per token group of 16 * NTT tokens and tile item (item = tile item
+// * groups + group), so consecutive items share the weight rows.
 // SPLIT: the two matrices read different token operands (in0 / in1).
 #ifndef DEAMOE_PF_NW1
 #define DEAMOE_PF_NW1 1
@@ -370,16 +374,23 @@ struct TileRunner {
     for (int n = 0; n < NW; ++n)
 #pragma unroll
       for (int tt = 0; tt < NTT; ++tt) acc[n][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    int rt0 = 0, nsub = 1;
+    int rt0 = 0, nsub = 1, tok0 = 0;
     if (active) {
+      constexpr int GT = kTile * NTT;   // tokens of a group
+      const int groups = (uniform(U->ntok) + GT - 1) / GT;
+      if (groups > 1) {
+        tok0 = (item % groups) * GT;
+        item = item / groups;
+      }
       const int tpg = KS == 1 ? uniform(U->tpg) : 1;
       const int ntiles = (uniform(U->R) + TR - 1) / TR;
       rt0 = item * tpg;
       nsub = min(tpg, ntiles - rt0);
       auto done = [&](int rt, const f32x4 (&a)[NW][NTT]) {
-        tile_epilogue<NW, NTT, PAIR>(*U, rt, sigma, a);
+        tile_epilogue<NW, NTT, PAIR>(*U, rt, tok0, sigma, a);
       };
-      tile_loop<WT, NW, NTT, SPLIT, PF, PAIR>(*U, rt0, nsub, kp, KS, sm.buf[wave], acc, done);
+      tile_loop<WT, NW, NTT, SPLIT, PF, PAIR>(*U, rt0, nsub, kp, KS, tok0, sm.buf[wave], acc,
+                                              done);
     }
     if constexpr (KS > 1) {
       f32x4 *red = reinterpret_cast<f32x4 *>(sm.buf[wave]);
@@ -401,7 +412,7 @@ struct TileRunner {
       }
       __syncthreads();
     }
-    if (active && kp == 0 && nsub == 1) tile_epilogue<NW, NTT, PAIR>(*U, rt0, sigma, acc);
+    if (active && kp == 0 && nsub == 1) tile_epilogue<NW, NTT, PAIR>(*U, rt0, tok0, sigma, acc);
   }
 };
 

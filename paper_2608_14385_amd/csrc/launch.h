@@ -39,6 +39,7 @@ struct RouteArgs {
   int32_t h, d_s, d_p, d_se, act_f32, w_bytes, fp8, plan;
   int32_t down_rows;     // weight rows of a down-projection tile (16, or 32 for row pairs)
   int32_t down_ks;       // waves sharing one down-projection tile (K split)
+  int32_t wave_tokens;   // tokens of one token group of the expert stages (16 * NTT)
   // logits: sum of kc partial products, or injected; optional bias
   const float *part;
   int32_t kc, ldp;

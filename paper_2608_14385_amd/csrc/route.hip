@@ -166,6 +166,63 @@ __device__ int block_exscan(int32_t *s, int N, int32_t *s_tmp) {
   return total;
 }
 
+// Exclusive prefix sums of two arrays a[0..N) and b[0..N) in place, in one
+// pass (shared barriers); returns both totals.  Every thread of the block
+// must call it; s_tmp holds 2 * (blockDim / 64) values.
+__device__ int2 block_exscan2(int32_t *a, int32_t *b, int N, int32_t *s_tmp) {
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
+  const int nwaves = nt / 64;
+  const int per = (N + nt - 1) / nt;
+  const int lo = min(tid * per, N), hi = min(lo + per, N);
+  int la = 0, lb = 0;
+  for (int i = lo; i < hi; ++i) {
+    la += a[i];
+    lb += b[i];
+  }
+  int va = la, vb = lb;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int oa = __shfl_up(va, off), ob = __shfl_up(vb, off);
+    if (lane >= off) {
+      va += oa;
+      vb += ob;
+    }
+  }
+  if (lane == 63) {
+    s_tmp[wave] = va;
+    s_tmp[32 + wave] = vb;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    int wa = lane < nwaves ? s_tmp[lane] : 0, wb = lane < nwaves ? s_tmp[32 + lane] : 0;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int oa = __shfl_up(wa, off), ob = __shfl_up(wb, off);
+      if (lane >= off) {
+        wa += oa;
+        wb += ob;
+      }
+    }
+    if (lane < nwaves) {
+      s_tmp[lane] = wa;
+      s_tmp[32 + lane] = wb;
+    }
+  }
+  __syncthreads();
+  int ra = (wave > 0 ? s_tmp[wave - 1] : 0) + va - la;
+  int rb = (wave > 0 ? s_tmp[32 + wave - 1] : 0) + vb - lb;
+  for (int i = lo; i < hi; ++i) {
+    const int xa = a[i], xb = b[i];
+    a[i] = ra;
+    b[i] = rb;
+    ra += xa;
+    rb += xb;
+  }
+  const int2 total = make_int2(s_tmp[nwaves - 1], s_tmp[32 + nwaves - 1]);
+  __syncthreads();
+  return total;
+}
+
 __device__ inline void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -579,7 +636,12 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       a.slot_pair[(size_t)t * S + s_nd[t] + (exp_slots ? k : 0)] = ndp + (slice ? nep_priv : 0) + t;
 
   // unit tables: unit index of an active department / expert = number of
-  // active ones before it
+  // active ones before it.  A unit's work items are its row-tile items times
+  // its token groups (wave_tokens tokens each).  Item prefixes over the units
+  // in table order are closed forms while no unit has more than one group;
+  // otherwise they come from block scans over an array with every
+  // department's items, then every expert's (the expert bitmaps' LDS, free
+  // after the placement above).
   const int wb = a.w_bytes, ab = a.act_f32 ? 4 : 2;
   const char *x = static_cast<const char *>(a.x);
   auto wptr = [&](const void *base, int idx, int R, int C) -> const void * {
@@ -590,12 +652,62 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
     return base + (size_t)idx * ((R + 127) / 128) * (C / 128);
   };
   const deamoe_weights &W = a.w;
+  const int wt = a.wave_tokens;
+  const bool multi = T > wt;
+  auto groups = [&](int cnt) { return multi ? (cnt + wt - 1) / wt : 1; };
+  int32_t *s_ia = reinterpret_cast<int32_t *>(s_etok);           // [m + n] items, stage pair A
+  int32_t *s_ib = s_ia + kMaxM + kMaxN;                           // [m + n] items, stage pair B
+  const int dr = a.down_rows, dk = a.down_ks;
+  // items per row-tile item: (A dept, A expert, B dept, B expert)
+  int ia_d, ia_e, ib_d, ib_e;
   if (slice) {
-    const int ta_d = (a.d_s + kTile - 1) / kTile, ta_p = (a.d_p + kTile - 1) / kTile;
-    const int dr = a.down_rows, dk = a.down_ks;
+    const int gd = tiles_per_item(a.d_s, dr, dk), gp = a.d_p ? tiles_per_item(a.d_p, dr, dk) : 1;
+    ia_d = (a.d_s + kTile - 1) / kTile;
+    ia_e = has_priv ? (a.d_p + kTile - 1) / kTile : 0;
+    ib_d = items_of(a.h, gd, dr);
+    ib_e = has_priv ? items_of(a.h, gp, dr) : 0;
+  } else {
+    const int d = a.d_s;
+    const int gd = tiles_per_item(d, dr, dk), g2 = tiles_per_item(d, dr, dk);
+    ia_d = (d + kTile - 1) / kTile;   // stage 0: W_g, W_u
+    ia_e = ia_d;                      // stage 1: A_g, A_u
+    ib_d = items_of(a.h, gd, dr);     // stage 3: W_d^T
+    ib_e = items_of(d, g2, dr);       // stage 2: A_d^T
+  }
+  int tot_a = 0, tot_b = 0;
+  if (multi) {
+    __syncthreads();   // the expert bitmaps are no longer read
+    if (tid < m) {
+      s_ia[tid] = my_dc > 0 ? ia_d * groups(my_dc) : 0;
+      s_ib[tid] = my_dc > 0 ? ib_d * groups(my_dc) : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      const int e = tid + q * BT;
+      if (e < n) {
+        const bool act = has_priv && my_ec[q] > 0;
+        s_ia[m + e] = act ? ia_e * groups(my_ec[q]) : 0;
+        s_ib[m + e] = act ? ib_e * groups(my_ec[q]) : 0;
+      }
+    }
+    __syncthreads();
+    const int2 tot = block_exscan2(s_ia, s_ib, m + n, s_tmp);
+    tot_a = tot.x;
+    tot_b = tot.y;
+  } else {
+    tot_a = ud * ia_d + ue * ia_e;
+    tot_b = ud * ib_d + ue * ib_e;
+  }
+  // first item of department j / expert e (unit index uj / ue_e) in each pair
+  auto dbeg_a = [&](int j, int uj) { return multi ? s_ia[j] : uj * ia_d; };
+  auto dbeg_b = [&](int j, int uj) { return multi ? s_ib[j] : uj * ib_d; };
+  auto ebeg_a = [&](int e, int ui) { return multi ? s_ia[m + e] : ud * ia_d + ui * ia_e; };
+  auto ebeg_b = [&](int e, int ui) { return multi ? s_ib[m + e] : ud * ib_d + ui * ib_e; };
+  const int dept_a = multi ? s_ia[m] : ud * ia_d;   // items of all departments
+  const int dept_b = multi ? s_ib[m] : ud * ib_d;
+  if (slice) {
     const int gd = tiles_per_item(a.d_s, dr, dk), gp = a.d_p ? tiles_per_item(a.d_p, dr, dk) : 1;
     const int gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
-    const int bd = items_of(a.h, gd, dr), bp = items_of(a.h, gp, dr);
     const int bse = items_of(a.h, gse, dr);
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_scan[j] >> 16, off = doff(j);
@@ -603,11 +715,11 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       char *ao = static_cast<char *>(a.abuf_dept) + (size_t)off * a.d_s * ab;
       put_unit(&a.units[0][u], wptr(W.dept_gate, j, a.d_s, a.h), wptr(W.dept_up, j, a.d_s, a.h),
                sptr(W.scale[0], j, a.d_s, a.h), sptr(W.scale[1], j, a.d_s, a.h), x, x, idx, ao,
-               nullptr, a.d_s, a.h, a.h, a.d_s, my_dc, u * ta_d, EPI_SWIGLU, a.act_f32);
+               nullptr, a.d_s, a.h, a.h, a.d_s, my_dc, dbeg_a(j, u), EPI_SWIGLU, a.act_f32);
       put_unit(&a.units[1][u], wptr(W.dept_down, j, a.h, a.d_s), nullptr,
                sptr(W.scale[2], j, a.h, a.d_s), nullptr, ao, ao, nullptr,
-               a.partial + (size_t)off * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, my_dc, u * bd,
-               EPI_STORE, 1, gd);
+               a.partial + (size_t)off * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, my_dc,
+               dbeg_b(j, u), EPI_STORE, 1, gd);
     }
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
@@ -618,37 +730,36 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       char *ao = static_cast<char *>(a.abuf_exp) + (size_t)off * a.d_p * ab;
       put_unit(&a.units[0][u], wptr(W.priv_gate, e, a.d_p, a.h), wptr(W.priv_up, e, a.d_p, a.h),
                sptr(W.scale[3], e, a.d_p, a.h), sptr(W.scale[4], e, a.d_p, a.h), x, x, idx, ao,
-               nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q], ud * ta_d + ui * ta_p, EPI_SWIGLU,
+               nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q], ebeg_a(e, ui), EPI_SWIGLU,
                a.act_f32);
       put_unit(&a.units[1][u], wptr(W.priv_down, e, a.h, a.d_p), nullptr,
                sptr(W.scale[5], e, a.h, a.d_p), nullptr, ao, ao, nullptr,
                a.partial + (size_t)(ndp + off) * a.h, nullptr, a.h, a.d_p, a.d_p, a.h, my_ec[q],
-               ud * bd + ui * bp, EPI_STORE, 1, gp);
+               ebeg_b(e, ui), EPI_STORE, 1, gp);
     }
     if (tid == 0) {
-      int units = ud + ue, tiles_a = ud * ta_d + ue * ta_p;
+      int units = ud + ue, items_a = tot_a, items_b = tot_b;
       if (has_se) {
         put_unit(&a.units[0][units], W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
-                 a.h, a.d_se, T, tiles_a, EPI_SWIGLU, a.act_f32);
+                 a.h, a.d_se, T, items_a, EPI_SWIGLU, a.act_f32);
         put_unit(&a.units[1][units], W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se), nullptr,
                  a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)(ndp + nep_priv) * a.h,
-                 nullptr, a.h, a.d_se, a.d_se, a.h, T, ud * bd + ue * bp, EPI_STORE, 1, gse);
-        tiles_a += (a.d_se + kTile - 1) / kTile;
+                 nullptr, a.h, a.d_se, a.d_se, a.h, T, items_b, EPI_STORE, 1, gse);
+        items_a += (a.d_se + kTile - 1) / kTile * groups(T);
+        items_b += bse * groups(T);
         ++units;
       }
       a.counts->stage[0][0] = units;
-      a.counts->stage[0][1] = tiles_a;
+      a.counts->stage[0][1] = items_a;
       a.counts->stage[1][0] = units;
-      a.counts->stage[1][1] = ud * bd + ue * bp + (has_se ? bse : 0);
+      a.counts->stage[1][1] = items_b;
     }
   } else {  // PLAN_FACTORED
-    const int d = a.d_s, td = (d + kTile - 1) / kTile;
-    const int dr = a.down_rows, dk = a.down_ks;
+    const int d = a.d_s;
     const int gd = tiles_per_item(d, dr, dk), gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
-    const int bd = items_of(a.h, gd, dr), bse = items_of(a.h, gse, dr);
-    // A_d^T: d x d, streamed like the down projections
-    const int g2 = tiles_per_item(d, dr, dk), b2 = items_of(d, g2, dr);
+    const int bse = items_of(a.h, gse, dr);
+    const int g2 = tiles_per_item(d, dr, dk);   // A_d^T: d x d, streamed like the down projections
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_scan[j] >> 16, off = doff(j);
       const int32_t *idx = a.r.dept_tokens + off;
@@ -657,10 +768,10 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       char *zs = static_cast<char *>(a.zsbuf) + (size_t)off * d * ab;
       put_unit(&a.units[0][u], wptr(W.dept_gate, j, d, a.h), wptr(W.dept_up, j, d, a.h),
                sptr(W.scale[0], j, d, a.h), sptr(W.scale[1], j, d, a.h), x, x, idx, go, uo, d,
-               a.h, a.h, d, my_dc, u * td, EPI_SIGMA2, a.act_f32);
+               a.h, a.h, d, my_dc, dbeg_a(j, u), EPI_SIGMA2, a.act_f32);
       put_unit(&a.units[3][u], wptr(W.dept_down, j, a.h, d), nullptr, sptr(W.scale[2], j, a.h, d),
                nullptr, zs, zs, nullptr, a.partial + (size_t)off * a.h, nullptr, a.h, d, d,
-               a.h, my_dc, u * bd, EPI_STORE, 1, gd);
+               a.h, my_dc, dbeg_b(j, u), EPI_STORE, 1, gd);
     }
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
@@ -670,33 +781,34 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       char *yo = static_cast<char *>(a.ybuf) + (size_t)off * d * ab;
       put_unit(&a.units[1][u], wptr(W.priv_gate, e, d, d), wptr(W.priv_up, e, d, d),
                sptr(W.scale[3], e, d, d), sptr(W.scale[4], e, d, d), a.gbuf, a.ubuf,
-               a.exp_src + off, yo, nullptr, d, d, d, d, my_ec[q], u * td, EPI_SWIGLU,
-               a.act_f32);
+               a.exp_src + off, yo, nullptr, d, d, d, d, my_ec[q], ebeg_a(e, u) - dept_a,
+               EPI_SWIGLU, a.act_f32);
       put_unit(&a.units[2][u], wptr(W.priv_down, e, d, d), nullptr, sptr(W.scale[5], e, d, d),
                nullptr, yo, yo, nullptr, a.zbuf + (size_t)off * d, nullptr, d, d, d, d,
-               my_ec[q], u * b2, EPI_SIGMA, 1, g2);
+               my_ec[q], ebeg_b(e, u) - dept_b, EPI_SIGMA, 1, g2);
     }
     if (tid == 0) {
-      int units0 = ud, tiles0 = ud * td, units3 = ud;
+      int units0 = ud, items0 = dept_a, units3 = ud, items3 = dept_b;
       if (has_se) {
         put_unit(&a.units[0][units0], W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
-                 a.h, a.d_se, T, tiles0, EPI_SWIGLU, a.act_f32);
+                 a.h, a.d_se, T, items0, EPI_SWIGLU, a.act_f32);
         put_unit(&a.units[3][units3], W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
                  nullptr, a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)ndp * a.h, nullptr,
-                 a.h, a.d_se, a.d_se, a.h, T, ud * bd, EPI_STORE, 1, gse);
+                 a.h, a.d_se, a.d_se, a.h, T, items3, EPI_STORE, 1, gse);
         ++units0;
-        tiles0 += (a.d_se + kTile - 1) / kTile;
+        items0 += (a.d_se + kTile - 1) / kTile * groups(T);
         ++units3;
+        items3 += bse * groups(T);
       }
       a.counts->stage[0][0] = units0;
-      a.counts->stage[0][1] = tiles0;
+      a.counts->stage[0][1] = items0;
       a.counts->stage[1][0] = ue;
-      a.counts->stage[1][1] = ue * td;
+      a.counts->stage[1][1] = tot_a - dept_a;
       a.counts->stage[2][0] = ue;
-      a.counts->stage[2][1] = ue * b2;
+      a.counts->stage[2][1] = tot_b - dept_b;
       a.counts->stage[3][0] = units3;
-      a.counts->stage[3][1] = ud * bd + (has_se ? bse : 0);
+      a.counts->stage[3][1] = items3;
     }
   }
   if (tid == 0) {
