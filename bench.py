@@ -79,6 +79,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--copies", type=int, default=0, help="weight copies (0: automatic)")
     ap.add_argument("--no-stages", action="store_true", help="skip the per-kernel event timing")
+    ap.add_argument("--layers", type=int, default=0,
+                    help="also time a decode step through this many distinct layers in one graph")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy 5 times (counter calibration)")
     return ap.parse_args()
@@ -220,6 +222,85 @@ class LayerRun:
             for q in e:
                 hip.destroy(q)
         return out
+
+
+class StackRun:
+    """A decode step through L distinct layers: layer i reads layer i - 1's
+    output (the attention and other non-MoE parts of a block are left out),
+    and the L calls are captured in one HIP graph and replayed."""
+
+    def __init__(self, cfg, L: int, T: int, baseline: bool, seed=0):
+        import torch
+        from paper_2608_14385_amd import deamoe as D
+        from paper_2608_14385_amd import workloads as W
+        self.D, self.torch, self.cfg, self.L, self.T = D, torch, cfg, L, T
+        self.weights = [W.make_weights(cfg, seed + 7919 * i, device="cuda") for i in range(L)]
+        self.structs = [D.make_weights(w) for w in self.weights]
+        self.c = D.make_config(cfg, T)
+        self.ws = D.alloc_workspace(self.c)
+        self.fn = D.lib().deamoe_baseline_forward if baseline else D.lib().deamoe_layer_forward
+        x0 = W.make_tokens(cfg, T, 500, device="cuda")
+        self.acts = [x0] + [torch.empty_like(x0) for _ in range(L)]
+        self.rts = [D.Routing.alloc(cfg, T) for _ in range(L)]
+        self.rstructs = [r.struct() for r in self.rts]
+
+    def step(self):
+        s = self.torch.cuda.current_stream().cuda_stream
+        for i in range(self.L):
+            rc = self.fn(C.byref(self.c), self.T, self.acts[i].data_ptr(), C.byref(self.structs[i]),
+                         None, None, C.byref(self.rstructs[i]), self.acts[i + 1].data_ptr(),
+                         self.ws.data_ptr(), self.ws.numel(), s)
+            if rc:
+                raise RuntimeError(f"layer call failed: {self.D.status_string(rc)}")
+
+    def step_bytes(self) -> int:
+        self.step()
+        self.torch.cuda.synchronize()
+        total = 0
+        for r in self.rts:
+            h = r.host()
+            total += self.D.deamoe_loaded_bytes(self.c, self.T, h["dept_count"], h["exp_count"])[1]
+        return total
+
+    def time_graph(self, reps: int, warmup: int) -> float:
+        torch = self.torch
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            self.step()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            self.step()
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+
+def multi_layer(cfg, base_cfg, L: int, T: int, reps: int) -> dict:
+    """DeaMoE and vanilla stacks of L layers at batch T (one after the other,
+    so only one stack's weights are resident at a time)."""
+    import torch
+    out = {"layers": L, "batch_tokens": T, "timing": "one HIP graph per decode step, replayed"}
+    for name, c, base in (("deamoe", cfg, False), ("vanilla", base_cfg, True)):
+        st = StackRun(c, L, T, base)
+        nbytes = st.step_bytes()
+        ms = st.time_graph(reps, 3)
+        out[name] = {"step_us": round(ms * 1e3, 2), "per_layer_us": round(ms * 1e3 / L, 2),
+                     "bytes_per_step": int(nbytes), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+        log(f"[bench] {L}-layer {name} T={T}: {out[name]}")
+        del st
+        torch.cuda.empty_cache()
+    out["speedup"] = round(out["vanilla"]["step_us"] / out["deamoe"]["step_us"], 3)
+    return out
 
 
 def stage_names(form: str) -> list:
@@ -373,6 +454,9 @@ def main():
         head = [r for r in sweep_rows if r["batch"] == T]
         if head and "speedup" in head[0]:
             result["speedup_vs_vanilla"] = head[0]["speedup"]
+
+    if args.layers > 0:
+        result["multi_layer"] = multi_layer(cfg, wl.baseline, args.layers, T, max(5, args.steps // 10))
 
     if args.copy_probe:
         src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")

@@ -175,7 +175,7 @@ int down_rows_of(int) { return DEAMOE_DOWN_PAIR ? 2 * kTile : kTile; }
 // FACTORED form (every contraction d long) splits K while the batch leaves
 // too few tiles to occupy the waves.
 int down_ks_of(const deamoe_config &c, int T) {
-  if (c.form == DEAMOE_FORM_SLICE) return DEAMOE_KS_DOWN;
+  if (c.form == DEAMOE_FORM_SLICE) return T <= DEAMOE_SDOWN_KS2_T ? 2 : DEAMOE_KS_DOWN;
   return T <= DEAMOE_FDOWN_KS4_T ? 4 : T <= DEAMOE_FDOWN_KS2_T ? 2 : 1;
 }
 

@@ -26,6 +26,11 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define DEAMOE_DOWN_PAIR 1
 #endif
 
+// SLICE down projections split K over 2 waves up to this many tokens (more
+// waves in flight while the batch leaves few work items).
+#ifndef DEAMOE_SDOWN_KS2_T
+#define DEAMOE_SDOWN_KS2_T 2
+#endif
 // K split of the FACTORED private gate/up stage (A_g G, A_u U).
 #ifndef DEAMOE_KS_FPRIV
 #define DEAMOE_KS_FPRIV 2
