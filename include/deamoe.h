@@ -12,7 +12,7 @@
  *     d_shared) plus a private SwiGLU slice (intermediate d_private), summed.
  *   Expert output, FACTORED form (Sec. 3.1, Eq. 4):
  *     d_i(g_i(x) * u_i(x)), g_i = SiLU(A_g sigma(W_g x)), u_i = A_u sigma(W_u x),
- *     d_i(v) = W_d^T sigma(A_d^T v), sigma = SiLU or identity.
+ *     d_i(v) = W_d^T sigma(A_d^T v), sigma = SiLU, identity, GeLU or RMSNorm.
  *   Layer output (Eq. 3): y = sum_{i in S(x)} p_i expert_i(x), plus an optional
  *     always-on shared SwiGLU expert with weight 1.
  *   Two-stage evaluation (Sec. 3.2): each touched department's shared
@@ -67,9 +67,12 @@ extern "C" {
 #define DEAMOE_SCORE_SOFTMAX 0
 #define DEAMOE_SCORE_SIGMOID 1
 
-/* interface nonlinearity sigma of the FACTORED form */
+/* interface nonlinearity sigma of the FACTORED form (Sec. 3.1; the
+ * alternatives are the ones compared in Sec. 3.4) */
 #define DEAMOE_SIGMA_SILU 0
-#define DEAMOE_SIGMA_NONE 1
+#define DEAMOE_SIGMA_NONE 1      /* identity                                            */
+#define DEAMOE_SIGMA_GELU 2      /* v * Phi(v), the exact (erf) form                     */
+#define DEAMOE_SIGMA_RMSNORM 3   /* v / sqrt(mean(v^2) + 1e-6) over the d-vector, unit gain */
 
 /* Limits of this build (DEAMOE_ERR_UNSUPPORTED beyond them). */
 #define DEAMOE_MAX_TOKENS 128
@@ -94,6 +97,12 @@ typedef struct {
   int32_t w_dtype;          /* expert weight type: DEAMOE_F32 | BF16 | FP8_E4M3_B128    */
   int32_t act_dtype;        /* x, y and router weight type: DEAMOE_F32 | DEAMOE_BF16    */
   int32_t max_tokens;       /* largest T the workspace is sized for (<= 128)            */
+  int32_t dept_cover;       /* 0: top_k_dept is an upper bound (group-limited top-k).
+                               1: strict coverage (Sec. 3.4): while a token's k experts
+                               span fewer than top_k_dept departments, its lowest-ranked
+                               expert whose department holds another selected expert is
+                               replaced by the best expert of a kept department not yet
+                               covered.  Needs top_k_dept > 0 and top_k >= top_k_dept. */
 } deamoe_config;
 
 /* Expert weights.  Shapes ([out, in], stacked):

@@ -5,7 +5,7 @@ Only tests/, the smoke check and the benchmark's CPU-baseline leg use it; the
 product path never does.  It takes plain tensors / arrays and any object with
 the layer-config attributes (hidden, n_experts, n_depts, top_k, top_k_dept,
 d_shared, d_private, d_shared_expert, form, score, renorm, sigma, route_scale,
-w_dtype, act_dtype); it imports nothing from the HIP package.
+w_dtype, act_dtype, optionally dept_cover); it imports nothing from the HIP package.
 """
 from __future__ import annotations
 
@@ -26,7 +26,8 @@ class _Config(C.Structure):
     _fields_ = [(f, C.c_int) for f in ("hidden", "n_experts", "n_depts", "top_k", "top_k_dept",
                                        "d_shared", "d_private", "d_shared_expert",
                                        "form", "score", "renorm", "sigma")] + \
-               [("route_scale", C.c_double), ("w_dtype", C.c_int), ("act_dtype", C.c_int)]
+               [("route_scale", C.c_double), ("w_dtype", C.c_int), ("act_dtype", C.c_int),
+                ("dept_cover", C.c_int)]
 
 
 class _Weights(C.Structure):
@@ -77,9 +78,10 @@ def _config(cfg) -> _Config:
                    d_private=cfg.d_private, d_shared_expert=cfg.d_shared_expert,
                    form={"slice": 0, "factored": 1}[cfg.form],
                    score={"softmax": 0, "sigmoid": 1}[cfg.score],
-                   renorm=int(bool(cfg.renorm)), sigma={"silu": 0, "none": 1}[cfg.sigma],
+                   renorm=int(bool(cfg.renorm)),
+                   sigma={"silu": 0, "none": 1, "gelu": 2, "rmsnorm": 3}[cfg.sigma],
                    route_scale=float(cfg.route_scale), w_dtype=_DT[cfg.w_dtype],
-                   act_dtype=_DT[cfg.act_dtype])
+                   act_dtype=_DT[cfg.act_dtype], dept_cover=int(getattr(cfg, "dept_cover", 0)))
 
 
 def _host(a, keep: list):

@@ -86,9 +86,23 @@ static void matvec(const mat_t *M, int idx, const double *v, double *out) {
 
 static double silu(double v) { return v / (1.0 + exp(-v)); }
 
-/* The interface nonlinearity sigma of the FACTORED form (Sec. 3.1, Sec. 3.4). */
-static double sigma_fn(const oref_config *cfg, double v) {
-  return cfg->sigma == OREF_SIGMA_NONE ? v : silu(v);
+/* GeLU in its exact form v * Phi(v), Phi the standard normal CDF. */
+static double gelu(double v) { return 0.5 * v * (1.0 + erf(v / sqrt(2.0))); }
+
+/* The interface nonlinearity sigma of the FACTORED form (Sec. 3.1; the
+ * variants compared in Sec. 3.4) applied in place to one d-vector.  SiLU,
+ * GeLU and the identity act per element; RMSNorm divides the whole vector by
+ * its root mean square (plus OREF_RMS_EPS), with unit gain. */
+static void sigma_vec(const oref_config *cfg, double *v, int d) {
+  if (cfg->sigma == OREF_SIGMA_NONE) return;
+  if (cfg->sigma == OREF_SIGMA_RMSNORM) {
+    double ss = 0.0;
+    for (int r = 0; r < d; ++r) ss += v[r] * v[r];
+    const double inv = 1.0 / sqrt(ss / d + OREF_RMS_EPS);
+    for (int r = 0; r < d; ++r) v[r] *= inv;
+    return;
+  }
+  for (int r = 0; r < d; ++r) v[r] = cfg->sigma == OREF_SIGMA_GELU ? gelu(v[r]) : silu(v[r]);
 }
 
 static void load_token(const oref_config *cfg, const void *x, int t, double *out) {
@@ -107,6 +121,9 @@ static int check_config(const oref_config *c) {
   if (c->top_k_dept < 0 || c->top_k_dept > c->n_depts) return -1;
   if (c->top_k_dept > 0 && c->top_k > c->top_k_dept * (c->n_experts / c->n_depts)) return -1;
   if (c->d_shared <= 0 || c->d_private < 0 || c->d_shared_expert < 0) return -1;
+  if (c->sigma < OREF_SIGMA_SILU || c->sigma > OREF_SIGMA_RMSNORM) return -1;
+  if (c->dept_cover != 0 && c->dept_cover != 1) return -1;
+  if (c->dept_cover && (c->top_k_dept == 0 || c->top_k < c->top_k_dept)) return -1;
   return 0;
 }
 
@@ -147,6 +164,34 @@ static void route_one(const oref_config *cfg, const float *l, int32_t *ids, doub
       if (allowed[e] && !taken[e] && (best < 0 || better(l[e], e, l[best], best))) best = e;
     taken[best] = 1;
     ids[r] = best;
+  }
+  if (cfg->dept_cover) {
+    /* strict coverage (Sec. 3.4): while the selection spans fewer than k_dept
+       departments, the lowest-ranked selected expert whose department keeps
+       another selected expert gives way to the best allowed expert of a
+       department not yet covered; the selection is then put back in rank
+       order.  Each round covers one more department. */
+    int *cnt = malloc(sizeof(int) * m);
+    for (;;) {
+      int D = 0;
+      memset(cnt, 0, sizeof(int) * m);
+      for (int r = 0; r < k; ++r) cnt[ids[r] / E] += 1;
+      for (int j = 0; j < m; ++j) D += cnt[j] > 0;
+      if (D >= cfg->top_k_dept) break;
+      int add = -1, victim = -1;
+      for (int e = 0; e < n; ++e)
+        if (allowed[e] && cnt[e / E] == 0 && (add < 0 || better(l[e], e, l[add], add))) add = e;
+      for (int r = k - 1; r >= 0 && victim < 0; --r)
+        if (cnt[ids[r] / E] >= 2) victim = r;
+      ids[victim] = add;
+      for (int r = 1; r < k; ++r)
+        for (int q = r; q > 0 && better(l[ids[q]], ids[q], l[ids[q - 1]], ids[q - 1]); --q) {
+          const int tmp = ids[q];
+          ids[q] = ids[q - 1];
+          ids[q - 1] = tmp;
+        }
+    }
+    free(cnt);
   }
   if (cfg->score == OREF_SOFTMAX) {
     double mx = -INFINITY, den = 0.0;
@@ -302,12 +347,13 @@ static void expert_out(const oref_config *cfg, const wset_t *s, int i, const dou
     double *a = malloc(sizeof(double) * d), *b = malloc(sizeof(double) * d);
     matvec(&s->M[0], j, x, G);
     matvec(&s->M[1], j, x, U);
-    for (int r = 0; r < d; ++r) { G[r] = sigma_fn(cfg, G[r]); U[r] = sigma_fn(cfg, U[r]); }
+    sigma_vec(cfg, G, d);
+    sigma_vec(cfg, U, d);
     matvec(&s->M[3], i, G, a);                     /* A_g sigma(W_g x)            */
     matvec(&s->M[4], i, U, b);                     /* A_u sigma(W_u x)            */
     for (int r = 0; r < d; ++r) a[r] = silu(a[r]) * b[r];   /* g_i(x) * u_i(x)   */
     matvec(&s->M[5], i, a, b);                     /* (A_d)^T v                   */
-    for (int r = 0; r < d; ++r) b[r] = sigma_fn(cfg, b[r]);
+    sigma_vec(cfg, b, d);                          /* sigma((A_d)^T v)            */
     matvec(&s->M[2], j, b, out);                   /* (W_d)^T sigma(...)          */
     free(G); free(U); free(a); free(b);
   } else {
@@ -420,10 +466,8 @@ int oref_layer_two_stage(const oref_config *cfg, int T, const void *x, const ore
         int t = R.dept_tokens[q];
         matvec(&s.M[0], j, X + (size_t)t * h, Xg + (size_t)t * d);
         matvec(&s.M[1], j, X + (size_t)t * h, Xu + (size_t)t * d);
-        for (int r = 0; r < d; ++r) {
-          Xg[(size_t)t * d + r] = sigma_fn(cfg, Xg[(size_t)t * d + r]);
-          Xu[(size_t)t * d + r] = sigma_fn(cfg, Xu[(size_t)t * d + r]);
-        }
+        sigma_vec(cfg, Xg + (size_t)t * d, d);
+        sigma_vec(cfg, Xu + (size_t)t * d, d);
         memset(Zj + (size_t)t * d, 0, sizeof(double) * d);
       }
       /* each expert of the department on its share of the tokens:
@@ -436,7 +480,8 @@ int oref_layer_two_stage(const oref_config *cfg, int T, const void *x, const ore
           matvec(&s.M[4], e, Xu + (size_t)t * d, b);
           for (int r = 0; r < d; ++r) a[r] = silu(a[r]) * b[r];
           matvec(&s.M[5], e, a, b);
-          for (int r = 0; r < d; ++r) Zj[(size_t)t * d + r] += pe * sigma_fn(cfg, b[r]);
+          sigma_vec(cfg, b, d);
+          for (int r = 0; r < d; ++r) Zj[(size_t)t * d + r] += pe * b[r];
         }
       /* O^j = (W_d^j)^T Z^j */
       for (int q = R.dept_offset[j]; q < R.dept_offset[j + 1]; ++q) {

@@ -27,7 +27,10 @@ extern "C" {
 enum { OREF_F32 = 0, OREF_BF16 = 1, OREF_FP8 = 2 };
 enum { OREF_SLICE = 0, OREF_FACTORED = 1 };
 enum { OREF_SOFTMAX = 0, OREF_SIGMOID = 1 };
-enum { OREF_SIGMA_SILU = 0, OREF_SIGMA_NONE = 1 };
+enum { OREF_SIGMA_SILU = 0, OREF_SIGMA_NONE = 1, OREF_SIGMA_GELU = 2, OREF_SIGMA_RMSNORM = 3 };
+
+/* RMSNorm variant of sigma: v / sqrt(mean(v^2) + eps) over the d-vector, unit gain. */
+#define OREF_RMS_EPS 1e-6
 
 typedef struct {
   int hidden, n_experts, n_depts, top_k, top_k_dept;
@@ -35,6 +38,8 @@ typedef struct {
   int form, score, renorm, sigma;
   double route_scale;
   int w_dtype, act_dtype;
+  int dept_cover;           /* 1: strict department coverage (Sec. 3.4), needs
+                               top_k_dept > 0 and top_k >= top_k_dept */
 } oref_config;
 
 /* Weight storage, row-major [out, in], stacked over departments / experts.

@@ -118,7 +118,9 @@ int validate_config(const deamoe_config *c) {
   if (c->form != DEAMOE_FORM_SLICE && c->form != DEAMOE_FORM_FACTORED) return DEAMOE_ERR_INVALID;
   if (c->score != DEAMOE_SCORE_SOFTMAX && c->score != DEAMOE_SCORE_SIGMOID) return DEAMOE_ERR_INVALID;
   if (c->renorm != 0 && c->renorm != 1) return DEAMOE_ERR_INVALID;
-  if (c->sigma != DEAMOE_SIGMA_SILU && c->sigma != DEAMOE_SIGMA_NONE) return DEAMOE_ERR_INVALID;
+  if (c->sigma < DEAMOE_SIGMA_SILU || c->sigma > DEAMOE_SIGMA_RMSNORM) return DEAMOE_ERR_INVALID;
+  if (c->dept_cover != 0 && c->dept_cover != 1) return DEAMOE_ERR_INVALID;
+  if (c->dept_cover && (c->top_k_dept == 0 || c->top_k < c->top_k_dept)) return DEAMOE_ERR_INVALID;
   if (!(c->route_scale == c->route_scale)) return DEAMOE_ERR_INVALID;
   if (c->w_dtype < DEAMOE_F32 || c->w_dtype > DEAMOE_FP8_E4M3_B128) return DEAMOE_ERR_INVALID;
   if (c->act_dtype != DEAMOE_F32 && c->act_dtype != DEAMOE_BF16) return DEAMOE_ERR_INVALID;
@@ -230,6 +232,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.m = c.n_depts;
   a.k = c.top_k;
   a.kdept = c.top_k_dept;
+  a.dept_cover = c.dept_cover;
   a.E = c.n_experts / c.n_depts;
   a.score = c.score;
   a.renorm = c.renorm;
@@ -368,6 +371,15 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     const int d = c.d_shared;
     const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
     DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, t0 * groups, kGridCap, s));
+    if (c.sigma == DEAMOE_SIGMA_RMSNORM) {   // timed with stage 0
+      RowNormArgs na;
+      na.counts = pc;
+      na.g = at<void>(ws, L.gbuf);
+      na.u = at<void>(ws, L.ubuf);
+      na.d = d;
+      na.act_f32 = c.act_dtype == DEAMOE_F32;
+      DEAMOE_TRY(launch_rownorm(na, T * dk, s));
+    }
     DEAMOE_TRY(ev.mark());
     DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, DEAMOE_KS_FPRIV,
                                    tiles_bound(act_exps, d) * groups, kGridCap, s));
@@ -388,6 +400,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     za.E = c.n_experts / m;
     za.d = d;
     za.act_f32 = c.act_dtype == DEAMOE_F32;
+    za.rms = c.sigma == DEAMOE_SIGMA_RMSNORM;
     DEAMOE_TRY(launch_zsum(za, T * dk, s));
     DEAMOE_TRY(ev.mark());
     DEAMOE_TRY(launch_down(stage(3), wt, T, down_ks_of(c, T), act_depts + se, c.hidden, kGridCap,
@@ -482,7 +495,7 @@ int deamoe_baseline_forward(const deamoe_config *cfg, int32_t T, const void *x,
                             void *ws, size_t ws_bytes, void *stream) {
   if (!cfg) return DEAMOE_ERR_INVALID;
   if (cfg->n_depts != cfg->n_experts || cfg->d_private != 0 || cfg->form != DEAMOE_FORM_SLICE ||
-      cfg->top_k_dept != 0)
+      cfg->top_k_dept != 0 || cfg->dept_cover != 0)
     return DEAMOE_ERR_INVALID;
   return layer_impl(cfg, T, x, w, logits_in, router_bias, routing_out, y, ws, ws_bytes, stream,
                     nullptr, 0);

@@ -74,6 +74,21 @@ __global__ __launch_bounds__(256) void zsum_kernel(ZsumArgs a) {
   }
   __syncthreads();
   const int n = s_n;
+  if (a.rms) {   // RMSNorm sigma: fold 1 / rms of each Z row into its weight
+    const int wv = threadIdx.x / 64, lane = threadIdx.x % 64;
+    for (int s = wv; s < n; s += blockDim.x / 64) {
+      const float *zr = a.z + (size_t)s_pair[s] * a.d;
+      float ss = 0.f;
+      for (int c = lane * 4; c < a.d; c += 256) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(zr + c);
+        ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+      if (lane == 0) s_w[s] = s_w[s] / sqrtf(ss / (float)a.d + kRmsEps);
+    }
+    __syncthreads();
+  }
   for (int c = threadIdx.x * 4; c < a.d; c += blockDim.x * 4) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s0 = 0; s0 < n; s0 += U) {
@@ -96,6 +111,60 @@ __global__ __launch_bounds__(256) void zsum_kernel(ZsumArgs a) {
           u32x2{lo, hi};
     }
   }
+}
+
+// One workgroup per department pair (pairs past the step's count return at
+// once): the sum of squares of the pair's g and u rows, then both rows
+// rescaled in place.
+__global__ __launch_bounds__(256) void rownorm_kernel(RowNormArgs a) {
+  __shared__ float s_part[2][4];
+  const int q = blockIdx.x;
+  if (q >= a.counts->n_dept_pairs) return;
+  const int wv = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const size_t base = (size_t)q * a.d;
+  auto at = [&](const void *p, int c) {
+    return a.act_f32 ? static_cast<const float *>(p)[base + c]
+                     : bf16_to_f32(static_cast<const uint16_t *>(p)[base + c]);
+  };
+  float sg = 0.f, su = 0.f;
+  for (int c = threadIdx.x; c < a.d; c += blockDim.x) {
+    const float g = at(a.g, c), u = at(a.u, c);
+    sg += g * g;
+    su += u * u;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    sg += __shfl_xor(sg, off);
+    su += __shfl_xor(su, off);
+  }
+  if (lane == 0) {
+    s_part[0][wv] = sg;
+    s_part[1][wv] = su;
+  }
+  __syncthreads();
+  float tg = 0.f, tu = 0.f;
+  for (int w = 0; w < (int)blockDim.x / 64; ++w) {
+    tg += s_part[0][w];
+    tu += s_part[1][w];
+  }
+  const float ig = 1.0f / sqrtf(tg / (float)a.d + kRmsEps);
+  const float iu = 1.0f / sqrtf(tu / (float)a.d + kRmsEps);
+  for (int c = threadIdx.x; c < a.d; c += blockDim.x) {
+    const float g = at(a.g, c) * ig, u = at(a.u, c) * iu;
+    if (a.act_f32) {
+      static_cast<float *>(a.g)[base + c] = g;
+      static_cast<float *>(a.u)[base + c] = u;
+    } else {
+      static_cast<uint16_t *>(a.g)[base + c] = f32_to_bf16(g);
+      static_cast<uint16_t *>(a.u)[base + c] = f32_to_bf16(u);
+    }
+  }
+}
+
+hipError_t launch_rownorm(const RowNormArgs &a, int max_dept_pairs, hipStream_t s) {
+  hipLaunchKernelGGL(rownorm_kernel, dim3(max_dept_pairs > 0 ? max_dept_pairs : 1), dim3(256), 0,
+                     s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_zsum(const ZsumArgs &a, int max_dept_pairs, hipStream_t s) {

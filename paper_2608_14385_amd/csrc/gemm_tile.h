@@ -284,8 +284,11 @@ __device__ inline void store4(void *base, int out_f32, size_t off, f32x4 o, bool
   }
 }
 
+// Element-wise part of sigma.  RMSNorm needs the whole d-vector: its stages
+// store the raw value and a row pass (rownorm_kernel, zsum_kernel) divides
+// by the root mean square.
 __device__ inline float apply_sigma(float v, int sigma) {
-  return sigma == DEAMOE_SIGMA_NONE ? v : silu_f(v);
+  return sigma == DEAMOE_SIGMA_SILU ? silu_f(v) : sigma == DEAMOE_SIGMA_GELU ? gelu_f(v) : v;
 }
 
 __device__ inline f32x4 sigma4(f32x4 v, int sigma) {

@@ -97,6 +97,10 @@ __device__ inline uint16_t f32_to_bf16(float f) {
 }
 
 __device__ inline float silu_f(float v) { return v / (1.0f + __expf(-v)); }
+// GeLU in its exact form v * Phi(v) = v / 2 * (1 + erf(v / sqrt 2)).
+__device__ inline float gelu_f(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
+// RMSNorm form of sigma: v / sqrt(mean(v^2) + kRmsEps) over a d-vector, unit gain.
+constexpr float kRmsEps = 1e-6f;
 
 __device__ inline int lane_id() { return __lane_id(); }
 

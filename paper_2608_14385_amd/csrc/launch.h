@@ -35,6 +35,7 @@ enum PlanMode : int32_t { PLAN_NONE = 0, PLAN_SLICE = 1, PLAN_FACTORED = 2 };
 struct RouteArgs {
   // configuration
   int32_t T, n, m, k, kdept, E, score, renorm;
+  int32_t dept_cover;    // strict coverage of exactly kdept departments
   float route_scale;
   int32_t h, d_s, d_p, d_se, act_f32, w_bytes, fp8, plan;
   int32_t down_rows;     // weight rows of a down-projection tile (16, or 32 for row pairs)
@@ -76,9 +77,20 @@ struct ZsumArgs {
   const float *topk_w, *z;
   void *zs;
   int32_t m, k, E, d, act_f32;
+  int32_t rms;           // sigma = RMSNorm: each Z row is divided by its root mean square
+};
+
+// sigma = RMSNorm at the gate / up interface of the FACTORED form: rows
+// [0, n_dept_pairs) of g and u, each of length d, divided in place by their
+// root mean square.
+struct RowNormArgs {
+  const PlanCounts *counts;
+  void *g, *u;
+  int32_t d, act_f32;
 };
 
 hipError_t launch_router(const RouterArgs &a, int wtype, int ntt, int kc, hipStream_t s);
+hipError_t launch_rownorm(const RowNormArgs &a, int max_dept_pairs, hipStream_t s);
 // The per-token kernel (grid T) followed by the plan kernel (one workgroup).
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 // Token-operand modes of two-matrix stages (nw == 2).

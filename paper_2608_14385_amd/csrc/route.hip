@@ -65,9 +65,12 @@ __device__ inline bool ranks_before(float va, int a, float vb, int b) {
   return va > vb || (va == vb && a < b);
 }
 
-// Order-preserving map of a float onto an unsigned int (larger float, larger key).
+// Order-preserving map of a float onto an unsigned int (larger float, larger
+// key).  -0 takes the key of +0: the two are equal values, so a tie between
+// them goes to the lower expert id like any other tie.
 __device__ inline uint32_t ord_u32(float f) {
-  const uint32_t u = __float_as_uint(f);
+  uint32_t u = __float_as_uint(f);
+  u = u == 0x80000000u ? 0u : u;
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
@@ -448,7 +451,45 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
   }
   wave_lds_sync();
   const bool sel = lane < k;
-  const uint64_t kk = sel ? s_ord[lane] : 0ull;
+  uint64_t kk = sel ? s_ord[lane] : 0ull;
+  // Strict coverage (Sec. 3.4).  While the k winners span fewer than kdept
+  // departments, the lowest-ranked winner whose department holds another
+  // winner gives way to the best eligible expert (key != 0: a kept
+  // department) of a department not yet covered, and the winners are ranked
+  // again.  Each round covers one more department.
+  if (a.dept_cover) {
+    for (int it = 0; it < a.kdept; ++it) {
+      const int dl = sel ? (int)(~(uint32_t)kk) / E : 0;
+      uint64_t cov = 0;
+      int mult = 0;
+      for (int q = 0; q < k; ++q) {
+        const int dq = __builtin_amdgcn_readlane(dl, q);
+        cov |= 1ull << (dq & 63);
+        mult += dq == dl;
+      }
+      if (popc64(cov) >= a.kdept) break;
+      uint64_t best = 0;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const int e = e0 + s;
+        const uint64_t c = ((uint64_t)key[s] << 32) | (uint32_t)~(uint32_t)e;
+        if (key[s] != 0u && !((cov >> ((e / E) & 63)) & 1) && c > best) best = c;
+      }
+      best = wave_max_u64(best);
+      const uint64_t vm = __ballot(sel && mult >= 2);
+      if (vm == 0 || best == 0) break;   // not reached when k >= kdept
+      if (lane == 63 - __clzll(vm)) kk = best;
+      if (sel) s_ord[lane] = kk;
+      wave_lds_sync();
+      int rank = 0;
+      for (int j = 0; j < k; ++j) rank += s_ord[j] > kk;
+      wave_lds_sync();
+      if (sel) s_ord[rank] = kk;
+      wave_lds_sync();
+      kk = sel ? s_ord[lane] : 0ull;
+      wave_lds_sync();
+    }
+  }
   const int my_id = sel ? (int)~(uint32_t)kk : 0;
   const uint32_t ob = (uint32_t)(kk >> 32);
   const float my_l = __uint_as_float((ob & 0x80000000u) ? (ob & 0x7fffffffu) : ~ob);

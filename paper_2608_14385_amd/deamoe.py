@@ -20,7 +20,7 @@ OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
 F32, BF16, FP8_E4M3_B128 = 0, 1, 2
 FORM_SLICE, FORM_FACTORED = 0, 1
 SCORE_SOFTMAX, SCORE_SIGMOID = 0, 1
-SIGMA_SILU, SIGMA_NONE = 0, 1
+SIGMA_SILU, SIGMA_NONE, SIGMA_GELU, SIGMA_RMSNORM = 0, 1, 2, 3
 MAX_TOKENS = 128
 
 EXPORTS = ("deamoe_status_string", "deamoe_workspace_bytes", "deamoe_route",
@@ -39,7 +39,7 @@ class deamoe_config(C.Structure):
                                          "d_shared", "d_private", "d_shared_expert", "form",
                                          "score", "renorm", "sigma")] + \
                [("route_scale", C.c_float), ("w_dtype", C.c_int32), ("act_dtype", C.c_int32),
-                ("max_tokens", C.c_int32)]
+                ("max_tokens", C.c_int32), ("dept_cover", C.c_int32)]
 
 
 class deamoe_weights(C.Structure):
@@ -106,9 +106,11 @@ def make_config(cfg, max_tokens: int) -> deamoe_config:
                          form={"slice": FORM_SLICE, "factored": FORM_FACTORED}[cfg.form],
                          score={"softmax": SCORE_SOFTMAX, "sigmoid": SCORE_SIGMOID}[cfg.score],
                          renorm=int(bool(cfg.renorm)),
-                         sigma={"silu": SIGMA_SILU, "none": SIGMA_NONE}[cfg.sigma],
+                         sigma={"silu": SIGMA_SILU, "none": SIGMA_NONE, "gelu": SIGMA_GELU,
+                                "rmsnorm": SIGMA_RMSNORM}[cfg.sigma],
                          route_scale=float(cfg.route_scale), w_dtype=_DT[cfg.w_dtype],
-                         act_dtype=_DT[cfg.act_dtype], max_tokens=int(max_tokens))
+                         act_dtype=_DT[cfg.act_dtype], max_tokens=int(max_tokens),
+                         dept_cover=int(getattr(cfg, "dept_cover", 0)))
 
 
 _WKEYS = ("dept_gate", "dept_up", "dept_down", "priv_gate", "priv_up", "priv_down",

@@ -53,10 +53,11 @@ class LayerConfig:
     form: str = "slice"          # "slice" | "factored"
     score: str = "softmax"       # "softmax" | "sigmoid"
     renorm: bool = True
-    sigma: str = "silu"          # interface nonlinearity of the FACTORED form: "silu" | "none"
+    sigma: str = "silu"          # FACTORED interface nonlinearity: "silu" | "none" | "gelu" | "rmsnorm"
     route_scale: float = 1.0
     w_dtype: str = "f32"         # "f32" | "bf16" | "fp8"
     act_dtype: str = "f32"       # "f32" | "bf16"
+    dept_cover: int = 0          # 1: strict department coverage (exactly top_k_dept per token)
 
     @property
     def experts_per_dept(self) -> int:

@@ -82,15 +82,47 @@ def brute_route(cfg, l32: np.ndarray):
             allowed = [e // E in D for e in range(n)]
         S = brute_topk(l, cfg.top_k, allowed)
         sets.append(S)
-        ls = l[list(S)]
-        if cfg.score == "softmax":
-            w = scipy.special.softmax(ls) if cfg.renorm else scipy.special.softmax(l)[list(S)]
-        else:
-            w = scipy.special.expit(ls)
-            if cfg.renorm:
-                w = w / w.sum()
-        P[t, list(S)] = w * cfg.route_scale
+        P[t, list(S)] = route_weights(cfg, l, S)
     return sets, P
+
+
+def route_weights(cfg, l: np.ndarray, S) -> np.ndarray:
+    """Weights p_i of the selected experts S (Sec. 2.1) from the logits l [n]."""
+    ls = l[list(S)]
+    if cfg.score == "softmax":
+        w = scipy.special.softmax(ls) if cfg.renorm else scipy.special.softmax(l)[list(S)]
+    else:
+        w = scipy.special.expit(ls)
+        if cfg.renorm:
+            w = w / w.sum()
+    return w * cfg.route_scale
+
+
+def strict_cover_closed_form(cfg, l: np.ndarray) -> list:
+    """Strict department coverage (Sec. 3.4) in closed form, for one token.
+
+    The replacement rule removes, one at a time, the lowest-ranked expert
+    whose department holds another selected expert, and adds the best expert
+    of a department not yet covered.  Its result is therefore fixed without
+    iterating: every department's best selected expert stays (it is never the
+    lowest of a department with two), the k - k_dept best of the remaining
+    selected experts stay, and each kept department the soft selection leaves
+    uncovered contributes its own best expert.  Returns ids in rank order."""
+    E, kd, k = cfg.experts_per_dept, cfg.top_k_dept, cfg.top_k
+    rank = lambda e: (-l[e], e)
+    gs = np.array([l[j * E:(j + 1) * E].max() for j in range(cfg.n_depts)])
+    kept = brute_topk(gs, kd)
+    allowed = [e // E in kept for e in range(cfg.n_experts)]
+    soft = sorted(brute_topk(l, k, allowed), key=rank)
+    depts = {e // E for e in soft}
+    if len(depts) >= kd:
+        return soft
+    tops, rest, seen = [], [], set()
+    for e in soft:
+        (rest if e // E in seen else tops).append(e)
+        seen.add(e // E)
+    added = [min(range(j * E, (j + 1) * E), key=rank) for j in kept if j not in depts]
+    return sorted(tops + rest[:k - kd] + added, key=rank)
 
 
 def vanilla_dense(cfg, x, w, logits_in=None, bias=None) -> np.ndarray:
@@ -228,14 +260,17 @@ def check_routing_ties():
     cfg = small(n_experts=8, n_depts=4, top_k=3, top_k_dept=2)
     logits = torch.tensor([[1, 1, 1, 1, 1, 1, 1, 1],
                            [0, 2, 2, 0, 2, 0, 0, 2],
-                           [3, 0, 0, 3, 0, 0, 3, 3]], dtype=torch.float32)
-    r = oracle.route(cfg, None, None, logits_in=logits, T=3)
+                           [3, 0, 0, 3, 0, 0, 3, 3],
+                           [-0.0, 0, -0.0, -0.0, 0, 0, -0.0, 0]], dtype=torch.float32)
+    r = oracle.route(cfg, None, None, logits_in=logits, T=4)
     # token 0: all equal -> departments 0,1 -> experts 0,1,2
     assert list(r["topk_ids"][0]) == [0, 1, 2]
     # token 1: group scores (2,2,2,2) -> depts 0,1 -> experts 1,2 (l=2) then 0 (l=0, lowest id)
     assert list(r["topk_ids"][1]) == [1, 2, 0]
     # token 2: group scores (3,3,0,3) -> depts 0,1 -> experts 0,3 (l=3) then 1
     assert list(r["topk_ids"][2]) == [0, 3, 1]
+    # token 3: -0 and +0 are the same value, so the order is by id alone
+    assert list(r["topk_ids"][3]) == [0, 1, 2]
 
 
 def check_vanilla_dense():
@@ -363,22 +398,118 @@ def check_factored_sigma_limit():
     assert r < 2e-2, r
 
 
-def check_factored_identity_silu():
-    """Eq. 4 with A = I and sigma = SiLU on one token per expert:
-    W_d^T SiLU(SiLU(SiLU(W_g x)) * SiLU(W_u x)), evaluated with torch."""
-    cfg = small(form="factored", d_shared=16, n_experts=4, n_depts=4, top_k=1)
-    w = W.make_weights(cfg, seed=43, gate_exact=True, identity_private=True)
-    x = W.make_tokens(cfg, 6, seed=43, gate_exact=True)
-    X = x.double()
-    l32 = (X @ w["router"].double().T).float().numpy()
-    sets, P = brute_route(cfg, l32)
+# torch's own implementations of the interface nonlinearities (Sec. 3.4):
+# SiLU, the exact (erf) GeLU, and RMSNorm with unit gain over the d-vector.
+TORCH_SIGMA = {"silu": F.silu, "gelu": lambda v: F.gelu(v, approximate="none"),
+               "rmsnorm": lambda v: F.rms_norm(v, (v.shape[-1],), eps=1e-6),
+               "none": lambda v: v}
+
+
+def check_factored_identity_sigma():
+    """Eq. 4 with A = I on one token per expert, for each sigma:
+    W_d^T sigma(SiLU(sigma(W_g x)) * sigma(W_u x)), evaluated with torch's
+    SiLU / GeLU / RMSNorm."""
+    for si, sigma in enumerate(("silu", "gelu", "rmsnorm")):
+        cfg = small(form="factored", d_shared=16, n_experts=4, n_depts=4, top_k=1, sigma=sigma)
+        w = W.make_weights(cfg, seed=43 + si, gate_exact=True, identity_private=True)
+        x = W.make_tokens(cfg, 6, seed=43 + si, gate_exact=True)
+        X = x.double()
+        l32 = (X @ w["router"].double().T).float().numpy()
+        sets, P = brute_route(cfg, l32)
+        y = oracle.layer(cfg, x, w)
+        sg = TORCH_SIGMA[sigma]
+        for t in range(6):
+            e = sets[t][0]
+            g = F.silu(sg(w["dept_gate"][e].double() @ X[t]))
+            u = sg(w["dept_up"][e].double() @ X[t])
+            o = w["dept_down"][e].double() @ sg(g * u)
+            assert rel(y[t], (P[t, e] * o).numpy()) < 1e-12, (sigma, t)
+
+
+def check_factored_sigma_general():
+    """Eq. 4 with general private matrices for GeLU and RMSNorm, several
+    experts per token, against torch: sum_i p_i W_d^T sigma(A_d^T (SiLU(A_g
+    sigma(W_g x)) * A_u sigma(W_u x)))."""
+    for si, sigma in enumerate(("gelu", "rmsnorm")):
+        cfg = small(form="factored", d_shared=16, n_experts=8, n_depts=2, top_k=3, sigma=sigma)
+        w = W.make_weights(cfg, seed=47 + si, gate_exact=True)
+        x = W.make_tokens(cfg, 5, seed=47 + si, gate_exact=True)
+        X = x.double()
+        l32 = (X @ w["router"].double().T).float().numpy()
+        _, P = brute_route(cfg, l32)
+        E = cfg.experts_per_dept
+        sg = TORCH_SIGMA[sigma]
+        ref = np.zeros((5, cfg.hidden))
+        for t in range(5):
+            for e in np.nonzero(P[t])[0]:
+                j = e // E
+                g = F.silu(w["priv_gate"][e].double() @ sg(w["dept_gate"][j].double() @ X[t]))
+                u = w["priv_up"][e].double() @ sg(w["dept_up"][j].double() @ X[t])
+                z = sg(w["priv_down"][e].double() @ (g * u))
+                ref[t] += P[t, e] * (w["dept_down"][j].double() @ z).numpy()
+        y = oracle.layer(cfg, x, w)
+        assert rel(y, ref) < 1e-12, (sigma, rel(y, ref))
+        assert rel(oracle.layer_two_stage(cfg, x, w), ref) < 1e-12, sigma
+
+
+def check_rmsnorm_scale_invariance():
+    """sigma = RMSNorm makes the layer invariant (up to the 1e-6 epsilon) to
+    positive scalings of W_g, W_u and A_d^T: each feeds an RMSNorm directly.
+    GeLU and SiLU are not: a scaled W_g changes their output."""
+    cfg = small(form="factored", d_shared=16, sigma="rmsnorm")
+    w = W.make_weights(cfg, seed=49)
+    x = W.make_tokens(cfg, 6, seed=49)
+    sc = dict(w)
+    sc["dept_gate"], sc["dept_up"], sc["priv_down"] = (w["dept_gate"] * 8.0, w["dept_up"] * 0.25,
+                                                      w["priv_down"] * 3.0)
     y = oracle.layer(cfg, x, w)
-    for t in range(6):
-        e = sets[t][0]
-        g = F.silu(F.silu(w["dept_gate"][e].double() @ X[t]))
-        u = F.silu(w["dept_up"][e].double() @ X[t])
-        o = w["dept_down"][e].double() @ F.silu(g * u)
-        assert rel(y[t], (P[t, e] * o).numpy()) < 1e-12
+    assert rel(oracle.layer(cfg, x, sc), y) < 1e-5
+    for other in ("gelu", "silu"):
+        c2 = cfg.replace(sigma=other)
+        assert rel(oracle.layer(c2, x, sc), oracle.layer(c2, x, w)) > 1e-2, other
+
+
+def check_strict_coverage():
+    """Strict department coverage (Sec. 3.4): every token spans exactly k_dept
+    departments; a token the soft rule already spreads over k_dept keeps its
+    selection; otherwise the selection matches the closed form above, in rank
+    order, with weights recomputed over the final set.  Whether the added
+    expert is sought among the kept departments only or among all makes no
+    difference: the kept departments hold the largest department maxima, so
+    the best expert of any uncovered department lies in a kept one (ties
+    included, as both rules break them towards lower ids); the checks below
+    hold for either reading."""
+    cases = [small(n_experts=16, n_depts=4, top_k=3, top_k_dept=3, dept_cover=1),
+             small(n_experts=32, n_depts=8, top_k=6, top_k_dept=4, dept_cover=1, score="sigmoid"),
+             small(n_experts=24, n_depts=6, top_k=4, top_k_dept=4, dept_cover=1, renorm=False),
+             small(n_experts=16, n_depts=8, top_k=4, top_k_dept=3, dept_cover=1, score="sigmoid",
+                   renorm=False, route_scale=2.5)]
+    rng = np.random.default_rng(5)
+    changed = 0
+    for ci, cfg in enumerate(cases):
+        T = 40
+        l = rng.standard_normal((T, cfg.n_experts)).astype(np.float32)
+        l[T // 2:] = np.round(l[T // 2:] * 2.0) / 2.0          # ties in the second half
+        r = oracle.route(cfg, None, None, logits_in=l, T=T)
+        soft = oracle.route(cfg.replace(dept_cover=0), None, None, logits_in=l, T=T)
+        E = cfg.experts_per_dept
+        for t in range(T):
+            lt = l[t].astype(np.float64)
+            ids = list(r["topk_ids"][t])
+            assert len({e // E for e in ids}) == cfg.top_k_dept, (ci, t)
+            assert ids == strict_cover_closed_form(cfg, lt), (ci, t, ids)
+            if len({e // E for e in soft["topk_ids"][t]}) == cfg.top_k_dept:
+                assert ids == list(soft["topk_ids"][t])
+            else:
+                changed += 1
+            assert np.allclose(r["topk_w"][t], route_weights(cfg, lt, ids), rtol=1e-14, atol=0)
+            assert r["tok_ndept"][t] == cfg.top_k_dept
+    assert changed > 20, changed
+    # the layer follows the strict selection in both evaluation orders
+    cfg = cases[1].replace(hidden=64, d_shared=32, d_private=16)
+    w = W.make_weights(cfg, seed=48)
+    x = W.make_tokens(cfg, 7, seed=48)
+    assert rel(oracle.layer_two_stage(cfg, x, w), oracle.layer(cfg, x, w)) < 1e-12
 
 
 def check_invariants():
@@ -505,6 +636,7 @@ def check_fig2_loading_ratio():
 
 ALL_CHECKS = [check_fp8_decode, check_routing_bruteforce, check_routing_ties,
               check_vanilla_dense, check_slice_reduces_to_vanilla, check_two_stage_equals_naive,
-              check_factored_reductions, check_factored_sigma_limit, check_factored_identity_silu,
+              check_factored_reductions, check_factored_sigma_limit, check_factored_identity_sigma,
+              check_factored_sigma_general, check_rmsnorm_scale_invariance, check_strict_coverage,
               check_invariants, check_accounting_vs_storage, check_table1_accounting,
               check_fig2_loading_ratio]

@@ -71,6 +71,11 @@ def ws_status(c):
     (dict(w_dtype="f32"), D.ERR_UNSUPPORTED),                # fp32 weights with bf16 activations
     (dict(n_experts=4096, n_depts=32), D.ERR_UNSUPPORTED),
     (dict(top_k=40), D.ERR_UNSUPPORTED),
+    (dict(top_k_dept=4, dept_cover=1), D.OK),
+    (dict(dept_cover=1), D.ERR_INVALID),                     # strict coverage needs top_k_dept > 0
+    (dict(top_k_dept=9, n_depts=32, top_k=8, dept_cover=1), D.ERR_INVALID),   # k < k_dept
+    (dict(sigma="gelu"), D.OK),
+    (dict(sigma="rmsnorm"), D.OK),
 ])
 def test_config_validation(mut, expect):
     if mut == dict(top_k_dept=1):
@@ -85,6 +90,7 @@ def test_config_validation_struct_fields():
     for field, val, expect in [("max_tokens", 0, D.ERR_INVALID), ("max_tokens", 129, D.ERR_UNSUPPORTED),
                                ("form", 5, D.ERR_INVALID), ("score", 2, D.ERR_INVALID),
                                ("renorm", 3, D.ERR_INVALID), ("sigma", 9, D.ERR_INVALID),
+                               ("sigma", -1, D.ERR_INVALID), ("dept_cover", 2, D.ERR_INVALID),
                                ("w_dtype", 7, D.ERR_INVALID), ("act_dtype", 2, D.ERR_INVALID)]:
         c = cfg_c3()
         setattr(c, field, val)

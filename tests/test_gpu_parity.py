@@ -174,8 +174,9 @@ def test_deterministic_and_route_only():
 @pytest.mark.parametrize("preset", ["tiny_f32", "7b_bf16", "dsv3_bf16", "dsv3_factored"])
 def test_route_ties(preset, T):
     """Coarse injected logits: many exact ties, including every logit equal
-    (more candidates than one per lane, so the exact selection path runs) and
-    a few equal values at the top (the candidate path); the lower id wins."""
+    (more candidates than one per lane, so the exact selection path runs), a
+    few equal values at the top (the candidate path) and a row of +0 and -0,
+    which are equal values; the lower id wins."""
     cfg = P[preset].layer
     n = cfg.n_experts
     g = torch.Generator(device="cpu").manual_seed(5 + T)
@@ -183,8 +184,9 @@ def test_route_ties(preset, T):
     rows = [torch.full((n,), 0.5),                                  # all equal
             torch.round(u[1] * 4) / 4,                              # five levels
             torch.round(u[2] * 64) / 64,                            # 65 levels
-            torch.where(u[3] > 0.97, torch.tensor(2.0), u[3])]      # equal maxima
-    rows += [torch.round(u[t] * (1 + t)) / (1 + t) for t in range(4, T)]
+            torch.where(u[3] > 0.97, torch.tensor(2.0), u[3]),      # equal maxima
+            torch.where(u[4] > 0.5, torch.tensor(0.0), torch.tensor(-0.0))]   # +0 and -0 tie
+    rows += [torch.round(u[t] * (1 + t)) / (1 + t) for t in range(5, T)]
     logits = torch.stack(rows).to(torch.float32).contiguous()
     act = torch.float32 if cfg.act_dtype == "f32" else torch.bfloat16
     x = torch.zeros(T, cfg.hidden, dtype=act)
@@ -197,6 +199,64 @@ def test_route_ties(preset, T):
     torch.cuda.synchronize()
     ref = oracle.route(cfg, x, router, logits_in=logits, bias=None, T=T)
     compare_routing(rt.host(), ref, T, cfg.top_k)
+
+
+@pytest.mark.parametrize("kind", ["ties", "gaussian"])
+@pytest.mark.parametrize("preset", ["dsv3_factored", "qwen3_factored", "base7b_factored"])
+def test_route_strict_coverage(preset, kind):
+    """Strict department coverage (Sec. 3.4) on the Table 1 FACTORED shapes:
+    exactly top_k_dept departments per token, ids bit-exact with the oracle."""
+    cfg = P[preset].layer.replace(dept_cover=1)
+    n, T = cfg.n_experts, 40
+    g = torch.Generator(device="cpu").manual_seed(17)
+    u = torch.randn(T, n, generator=g)
+    if kind == "ties":
+        u = torch.round(u * torch.arange(1, T + 1).unsqueeze(1) / 8) / 4
+        u[0] = 0.5
+    logits = u.to(torch.float32).contiguous()
+    x = torch.zeros(T, cfg.hidden, dtype=torch.bfloat16)
+    router = torch.zeros(n, cfg.hidden, dtype=torch.bfloat16)
+    say(f"[gpu] strict coverage route {preset} {kind} T={T}")
+    c = D.make_config(cfg, T)
+    ws = D.alloc_workspace(c)
+    rt = D.Routing.alloc(cfg, T)
+    D.deamoe_route(c, x.cuda(), router.cuda(), rt, ws, logits_in=logits.cuda())
+    torch.cuda.synchronize()
+    ref = oracle.route(cfg, x, router, logits_in=logits, bias=None, T=T)
+    got = rt.host()
+    compare_routing(got, ref, T, cfg.top_k)
+    E = cfg.experts_per_dept
+    for t in range(T):
+        assert len(set((np.asarray(got["topk_ids"]).reshape(T, -1)[t] // E).tolist())) == \
+            cfg.top_k_dept
+
+
+@pytest.mark.parametrize("variant", ["small_f32", "dsv3_factored"])
+def test_layer_strict_coverage(variant):
+    if variant == "small_f32":
+        case = Case(small(n_experts=64, n_depts=8, top_k=6, top_k_dept=3, dept_cover=1,
+                          d_shared_expert=128), 21, seed=23)
+        check_case(case)
+    else:
+        case = Case(P["dsv3_factored"].layer.replace(dept_cover=1), 16, seed=24)
+        check_case(case, tokens=sample_tokens(16, 2))
+
+
+@pytest.mark.parametrize("sigma", ["gelu", "rmsnorm"])
+@pytest.mark.parametrize("variant", ["tiny", "group_limited_se", "dsv3_factored"])
+def test_factored_sigma(variant, sigma):
+    """The GeLU and RMSNorm interface nonlinearities of Sec. 3.4."""
+    if variant == "tiny":
+        case = Case(P["tiny_factored"].layer.replace(sigma=sigma), 19, seed=25)
+        check_case(case)
+    elif variant == "group_limited_se":
+        base = P["tiny_factored"].layer
+        case = Case(base.replace(n_experts=32, n_depts=4, top_k=5, top_k_dept=2,
+                                 d_shared_expert=128, score="sigmoid", sigma=sigma), 11, seed=26)
+        check_case(case)
+    else:
+        case = Case(P["dsv3_factored"].layer.replace(sigma=sigma), 16, seed=27)
+        check_case(case, tokens=sample_tokens(16, 2))
 
 
 def test_empty_batch_is_a_no_op():

@@ -18,8 +18,15 @@ MUTANTS = {
     "silu_sign": ("return v / (1.0 + exp(-v));", "return v / (1.0 + exp(v));"),
     "drop_private_slice": ("for (int c = 0; c < h; ++c) out[c] += q[c];",
                            "for (int c = 0; c < h; ++c) out[c] += 0.0 * q[c];"),
-    "sigma_missing_down": ("for (int r = 0; r < d; ++r) b[r] = sigma_fn(cfg, b[r]);",
-                           "for (int r = 0; r < d; ++r) b[r] = b[r];"),
+    "sigma_missing_down": ("sigma_vec(cfg, b, d);                          /* sigma((A_d)^T v)",
+                           "/* sigma((A_d)^T v)"),
+    "gelu_unscaled_erf": ("erf(v / sqrt(2.0))", "erf(v)"),
+    "rmsnorm_sum_not_mean": ("sqrt(ss / d + OREF_RMS_EPS)", "sqrt(ss + OREF_RMS_EPS)"),
+    "cover_one_short": ("if (D >= cfg->top_k_dept) break;", "if (D >= cfg->top_k_dept - 1) break;"),
+    "cover_victim_highest_rank": ("for (int r = k - 1; r >= 0 && victim < 0; --r)",
+                                  "for (int r = 0; r < k && victim < 0; ++r)"),
+    "cover_no_rerank": ("for (int r = 1; r < k; ++r)\n        for (int q = r;",
+                        "for (int r = k; r < k; ++r)\n        for (int q = r;"),
     "gate_up_swapped": ("matvec(&s->M[3], i, G, a);", "matvec(&s->M[4], i, G, a);"),
     "tie_break_high_id": ("(la == lb && a < b)", "(la == lb && a > b)"),
     "dept_of_expert_modulo": ("j = i / (cfg->n_experts / cfg->n_depts);",
