@@ -112,16 +112,52 @@ __device__ inline int wave_argmax_idx(float v, int i, bool valid, float &best_v)
   return (int)~(uint32_t)b;
 }
 
+// DPP exchange of a 32-bit value within rows of 16 lanes.
+template <int CTRL>
+__device__ inline float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL,
+                                                    0xf, 0xf, false));
+}
+
+// Wave-wide sum / maximum returned to every lane: butterflies within each row
+// of 16 lanes (xor 1, xor 2, half-row mirror, row mirror), then the four row
+// results through readlane, combined in row order.
 __device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-  return v;
+  v += dpp_f32<0xB1>(v);
+  v += dpp_f32<0x4E>(v);
+  v += dpp_f32<0x141>(v);
+  v += dpp_f32<0x140>(v);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return ((r0 + r1) + r2) + r3;
 }
 
 __device__ inline float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
-  return v;
+  v = fmaxf(v, dpp_f32<0xB1>(v));
+  v = fmaxf(v, dpp_f32<0x4E>(v));
+  v = fmaxf(v, dpp_f32<0x141>(v));
+  v = fmaxf(v, dpp_f32<0x140>(v));
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+
+// Inclusive prefix sum over the wave: shifts by 1, 2, 4, 8 within each row
+// of 16 lanes (lanes shifted in from outside the row add 0), then the row
+// totals below each lane's row through readlane.
+__device__ inline int wave_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+  const int lane = __lane_id();
+  const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31);
+  const int r2 = __builtin_amdgcn_readlane(v, 47);
+  return v + (lane >= 16 ? r0 : 0) + (lane >= 32 ? r1 : 0) + (lane >= 48 ? r2 : 0);
 }
 
 // Order-preserving float <-> int map for integer max.
@@ -140,21 +176,11 @@ __device__ int block_exscan(int32_t *s, int N, int32_t *s_tmp) {
   const int b = min(tid * per, N), e = min(b + per, N);
   int local = 0;
   for (int i = b; i < e; ++i) local += s[i];
-  int v = local;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int o = __shfl_up(v, off);
-    if (lane >= off) v += o;
-  }
+  const int v = wave_incl_scan(local);
   if (lane == 63) s_tmp[wave] = v;
   __syncthreads();
   if (wave == 0) {
-    int w = lane < nwaves ? s_tmp[lane] : 0;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int o = __shfl_up(w, off);
-      if (lane >= off) w += o;
-    }
+    const int w = wave_incl_scan(lane < nwaves ? s_tmp[lane] : 0);
     if (lane < nwaves) s_tmp[lane] = w;
   }
   __syncthreads();
@@ -182,30 +208,15 @@ __device__ int2 block_exscan2(int32_t *a, int32_t *b, int N, int32_t *s_tmp) {
     la += a[i];
     lb += b[i];
   }
-  int va = la, vb = lb;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int oa = __shfl_up(va, off), ob = __shfl_up(vb, off);
-    if (lane >= off) {
-      va += oa;
-      vb += ob;
-    }
-  }
+  const int va = wave_incl_scan(la), vb = wave_incl_scan(lb);
   if (lane == 63) {
     s_tmp[wave] = va;
     s_tmp[32 + wave] = vb;
   }
   __syncthreads();
   if (wave == 0) {
-    int wa = lane < nwaves ? s_tmp[lane] : 0, wb = lane < nwaves ? s_tmp[32 + lane] : 0;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int oa = __shfl_up(wa, off), ob = __shfl_up(wb, off);
-      if (lane >= off) {
-        wa += oa;
-        wb += ob;
-      }
-    }
+    const int wa = wave_incl_scan(lane < nwaves ? s_tmp[lane] : 0);
+    const int wb = wave_incl_scan(lane < nwaves ? s_tmp[32 + lane] : 0);
     if (lane < nwaves) {
       s_tmp[lane] = wa;
       s_tmp[32 + lane] = wb;
@@ -444,9 +455,17 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
   }
   wave_lds_sync();
   if (lane < ncand) {
+    // a batch of 8 LDS reads is issued before any is compared (entries past
+    // ncand are read but not counted)
     const uint64_t mine = s_sel[lane];
     int rank = 0;
-    for (int j = 0; j < ncand; ++j) rank += s_sel[j] > mine;
+    for (int j0 = 0; j0 < ncand; j0 += 8) {
+      uint64_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = s_sel[(j0 + u) & 63];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) rank += (j0 + u < ncand) & (v[u] > mine);
+    }
     if (rank < k) s_ord[rank] = mine;
   }
   wave_lds_sync();
@@ -499,7 +518,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
   if (a.score == DEAMOE_SCORE_SOFTMAX) {
     float mx, den;
     if (a.renorm) {
-      mx = __shfl(my_l, 0);
+      mx = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_l), 0));
       den = wave_sum(sel ? expf(my_l - mx) : 0.f);
     } else {
       float lm = -INFINITY;
