@@ -15,6 +15,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
   __shared__ typename Run::Smem sm;
   __shared__ int32_t s_begin[kMaxUnitsCached];
   const int n_units = st.counts[0], n_tiles = st.counts[1];
+  if (blockIdx.x * Run::TPB >= n_tiles) return;   // the grid is sized for the most work a step can have
   for (int u = threadIdx.x; u < n_units; u += blockDim.x) s_begin[u] = st.units[u].tile_begin;
   __syncthreads();
   const int wave = uniform(threadIdx.x / kWave);
