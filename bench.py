@@ -81,6 +81,8 @@ def parse():
     ap.add_argument("--no-stages", action="store_true", help="skip the per-kernel event timing")
     ap.add_argument("--layers", type=int, default=0,
                     help="also time a decode step through this many distinct layers in one graph")
+    ap.add_argument("--no-stream", action="store_true",
+                    help="skip the read-bandwidth probe (libdeamoe_probe.so)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy 5 times (counter calibration)")
     return ap.parse_args()
@@ -173,6 +175,21 @@ class LayerRun:
         b.record()
         torch.cuda.synchronize()
         return a.elapsed_time(b) / steps
+
+    def time_each(self, steps: int, warmup: int) -> np.ndarray:
+        """Per-step latencies (ms): an event before every step and one after
+        the last, all on the launch stream, steps launched back to back."""
+        torch = self.torch
+        for i in range(warmup):
+            self.step(i)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        torch.cuda.synchronize()
+        for i in range(steps):
+            evs[i].record()
+            self.step(i)
+        evs[steps].record()
+        torch.cuda.synchronize()
+        return np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)])
 
     def time_graph(self, steps: int, warmup: int) -> float:
         """Steps captured in one hipGraph (8 steps per graph), replayed."""
@@ -332,6 +349,66 @@ def gate_up_bytes(cfg, T: int, dept_count, exp_count) -> int:
     return b
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_single_core(run: LayerRun, T: int, hw: dict, min_seconds: float = 3.0) -> dict:
+    """The oracle on one thread, on single tokens of the step's token batches
+    (its cost is per token and expert), scaled to whole steps."""
+    import oracle
+    threads = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        done, t0 = 0, time.perf_counter()
+        while done < 4 * T and (done == 0 or time.perf_counter() - t0 < min_seconds):
+            i, t = (done // T) % len(run.xs), done % T
+            oracle.layer(run.cfg, run.xs[i].cpu(), hw, tokens=[t])
+            done += 1
+        dt = time.perf_counter() - t0
+    finally:
+        oracle.set_num_threads(threads)
+    step_s = dt / done * T
+    return {"value": float(np.mean([run.step_bytes(i) for i in range(len(run.xs))])) / step_s / 1e9,
+            "unit": "GB/s", "cores": 1, "sample": f"{done} single tokens at one thread, "
+            f"{dt:.1f}s, scaled to {T}-token steps", "seconds_per_step": step_s}
+
+
+def stream_read_peak(nbytes: int = 4 << 30, reps: int = 10) -> float:
+    """GB/s of the read probe (libdeamoe_probe.so) streaming a 4 GiB buffer."""
+    import torch
+    from paper_2608_14385_amd import build as B
+    lib = C.CDLL(B.PROBE_LIB)
+    lib.deamoe_probe_read.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_int, C.c_void_p]
+    bufs = [torch.ones(nbytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+
+    def go(i):
+        rc = lib.deamoe_probe_read(bufs[i % 2].data_ptr(), nbytes, sink.data_ptr(), 8192, s)
+        assert rc == 0, rc
+    for i in range(3):
+        go(i)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for i in range(reps):
+        go(i)
+    b.record()
+    torch.cuda.synchronize()
+    gbps = nbytes * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+    del bufs
+    torch.cuda.empty_cache()
+    return gbps
+
+
 def cpu_baseline(run: LayerRun, T: int, min_seconds: float = 10.0) -> dict:
     """The oracle on whole steps of the same workload (successive token
     batches) until at least `min_seconds` of CPU work, at most 16 steps."""
@@ -345,10 +422,13 @@ def cpu_baseline(run: LayerRun, T: int, min_seconds: float = 10.0) -> dict:
         nbytes += run.step_bytes(i)
         done += 1
     dt = time.perf_counter() - t0
-    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} whole {run.cfg.name} steps of {T} tokens (successive token "
-                      f"batches), naive fp64 per-token per-expert loop, {dt:.1f}s",
-            "seconds_per_step": dt / done}
+    out = {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+           "sample": f"{done} whole {run.cfg.name} steps of {T} tokens (successive token "
+                     f"batches), naive fp64 per-token per-expert loop, {dt:.1f}s",
+           "seconds_per_step": dt / done, "cpu_model": cpu_model(),
+           "affinity_cores": len(os.sched_getaffinity(0))}
+    out["single_core"] = cpu_single_core(run, T, hw)
+    return out
 
 
 def main():
@@ -395,6 +475,11 @@ def main():
         "batch_tokens": T, "weight_copies": len(run.copies), "token_batches": len(run.xs),
         "timing": "direct launches on one stream, torch.cuda events around all steps"}
     result["latency_us"] = round(ms * 1e3, 2)
+    each = run.time_each(args.steps, 5) * 1e3
+    result["latency_percentiles_us"] = {"p10": round(float(np.percentile(each, 10)), 2),
+                                        "p50": round(float(np.percentile(each, 50)), 2),
+                                        "p90": round(float(np.percentile(each, 90)), 2),
+                                        "timing": "an event before every step, steps back to back"}
     result["bytes_per_step"] = int(np.mean(step_bytes))
     result["hbm_frac"] = round(gbps / HBM_PEAK_GBPS, 4)
     log(f"[bench] {cfg.name} T={T}: {ms * 1e3:.1f} us/step, {gbps:.0f} GB/s")
@@ -457,6 +542,17 @@ def main():
 
     if args.layers > 0:
         result["multi_layer"] = multi_layer(cfg, wl.baseline, args.layers, T, max(5, args.steps // 10))
+
+    if not args.no_stream:
+        peak = stream_read_peak()
+        result["stream_read_peak"] = {
+            "GBps": round(peak, 1), "frac_of_peak": round(peak / HBM_PEAK_GBPS, 4),
+            "probe": "libdeamoe_probe.so: 4 GiB read once, 16-byte non-temporal loads, "
+                     "8192 workgroups of 256 lanes, 10 passes"}
+        if "roofline" in result:
+            result["stream_read_peak"]["gate_up_frac_of_stream"] = round(
+                result["roofline"]["achieved"] / peak, 4)
+        log(f"[bench] read probe: {peak:.0f} GB/s")
 
     if args.copy_probe:
         src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")

@@ -44,6 +44,7 @@ def _open(path: str):
     """Load an oracle build and declare its signatures."""
     L = C.CDLL(path)
     L.oref_num_threads.restype = C.c_int
+    L.oref_set_num_threads.argtypes = [C.c_int]
     L.oref_fp8_value.restype = C.c_double
     L.oref_fp8_value.argtypes = [C.c_uint8]
     L.oref_fp8_decode.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p]
@@ -181,6 +182,11 @@ def layer_two_stage(cfg, x, weights: dict, logits_in=None, bias=None) -> np.ndar
     if rc:
         raise ValueError("oracle rejected the configuration")
     return y
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the naive layer's token loop for later calls."""
+    lib().oref_set_num_threads(int(n))
 
 
 def num_threads() -> int:

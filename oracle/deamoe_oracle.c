@@ -30,6 +30,7 @@
 #include <string.h>
 
 int oref_num_threads(void) { return omp_get_max_threads(); }
+void oref_set_num_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
 
 /* ---------------------------------------------------------------- decoding */
 

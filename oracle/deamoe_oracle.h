@@ -71,8 +71,10 @@ typedef struct {
   int32_t *exp_count, *exp_offset, *exp_tokens;      /* [n], [n+1], [T*k]      */
 } oref_routing;
 
-/* Threads the token loops of oref_layer_naive may use (OpenMP). */
+/* Threads the token loops of oref_layer_naive may use (OpenMP); the setter
+ * changes it for later calls from the calling thread. */
 int oref_num_threads(void);
+void oref_set_num_threads(int n);
 
 /* e4m3fn (OCP) code -> value. */
 double oref_fp8_value(uint8_t code);

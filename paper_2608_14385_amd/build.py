@@ -1,4 +1,5 @@
-"""Build libdeamoe.so (HIP, gfx950) in-tree with hipcc.
+"""Build libdeamoe.so (HIP, gfx950) in-tree with hipcc, and the benchmark's
+read-bandwidth probe libdeamoe_probe.so.
 
     python -m paper_2608_14385_amd.build
 """
@@ -14,6 +15,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdeamoe.so")
 SOURCES = ("api.hip", "route.hip", "gemm.hip", "combine.hip")
+PROBE_SRC = os.path.join(CSRC, "probe", "read_probe.hip")
+PROBE_LIB = os.path.join(HERE, "libdeamoe_probe.so")
 
 # Packed fp32 instructions are disabled for all device code.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
@@ -25,7 +28,7 @@ def _hipcc() -> str:
 
 
 def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+    obj = os.path.join(BUILD, os.path.basename(src).replace(".hip", ".o"))
     cmd = [_hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
@@ -48,6 +51,10 @@ def build(verbose: bool = False) -> str:
     cmd = [_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     subprocess.run(cmd, check=True, capture_output=not verbose)
     os.replace(tmp, LIB)
+    probe = _compile(PROBE_SRC, verbose)
+    cmd = [_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", PROBE_LIB + ".tmp", probe]
+    subprocess.run(cmd, check=True, capture_output=not verbose)
+    os.replace(PROBE_LIB + ".tmp", PROBE_LIB)
     return LIB
 
 

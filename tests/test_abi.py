@@ -230,3 +230,10 @@ def test_loaded_bytes_monte_carlo_matches_closed_form():
             tot_v += D.deamoe_loaded_bytes(cv, T, vc, vc)[0]
         assert abs(tot_d / tot_v - oracle_pins.expected_ratio(T)) < 0.01, T
     assert E == 108
+
+
+def test_read_probe_library_exports():
+    """The benchmark's read-bandwidth probe loads and exports its one entry point."""
+    from paper_2608_14385_amd import build as B
+    lib = C.CDLL(B.PROBE_LIB)
+    assert hasattr(lib, "deamoe_probe_read")
