@@ -13,6 +13,8 @@
 //   ascending token order (no atomics on any order-sensitive value), the
 //   unit tables of every expert stage (pointers, row-tile prefix), the
 //   combine slots of every token, and the counts.
+// route_plan_kernel: both of the above in one workgroup for batches of up
+//   to four tokens, the per-token results passed on through LDS.
 #include "gemm_tile.h"
 #include "launch.h"
 
@@ -167,6 +169,16 @@ __device__ inline int ord_key(float f) {
 }
 __device__ inline float ord_val(int i) { return __int_as_float(i >= 0 ? i : i ^ 0x7fffffff); }
 
+// Workgroup barrier that orders LDS accesses only: global stores issued
+// before it may still be in flight.  The route and plan kernels never read
+// back, within a launch, global data they wrote, so their barriers need no
+// more (a full barrier would wait for every outstanding store).
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Exclusive prefix sum of s[0..N) in place, N <= 4 * blockDim; returns the
 // total.  Every thread of the block must call it.
 __device__ int block_exscan(int32_t *s, int N, int32_t *s_tmp) {
@@ -178,12 +190,12 @@ __device__ int block_exscan(int32_t *s, int N, int32_t *s_tmp) {
   for (int i = b; i < e; ++i) local += s[i];
   const int v = wave_incl_scan(local);
   if (lane == 63) s_tmp[wave] = v;
-  __syncthreads();
+  lds_barrier();
   if (wave == 0) {
     const int w = wave_incl_scan(lane < nwaves ? s_tmp[lane] : 0);
     if (lane < nwaves) s_tmp[lane] = w;
   }
-  __syncthreads();
+  lds_barrier();
   int run = (wave > 0 ? s_tmp[wave - 1] : 0) + v - local;
   for (int i = b; i < e; ++i) {
     const int x = s[i];
@@ -191,7 +203,7 @@ __device__ int block_exscan(int32_t *s, int N, int32_t *s_tmp) {
     run += x;
   }
   const int total = s_tmp[nwaves - 1];
-  __syncthreads();
+  lds_barrier();
   return total;
 }
 
@@ -213,7 +225,7 @@ __device__ int2 block_exscan2(int32_t *a, int32_t *b, int N, int32_t *s_tmp) {
     s_tmp[wave] = va;
     s_tmp[32 + wave] = vb;
   }
-  __syncthreads();
+  lds_barrier();
   if (wave == 0) {
     const int wa = wave_incl_scan(lane < nwaves ? s_tmp[lane] : 0);
     const int wb = wave_incl_scan(lane < nwaves ? s_tmp[32 + lane] : 0);
@@ -222,7 +234,7 @@ __device__ int2 block_exscan2(int32_t *a, int32_t *b, int N, int32_t *s_tmp) {
       s_tmp[32 + lane] = wb;
     }
   }
-  __syncthreads();
+  lds_barrier();
   int ra = (wave > 0 ? s_tmp[wave - 1] : 0) + va - la;
   int rb = (wave > 0 ? s_tmp[32 + wave - 1] : 0) + vb - lb;
   for (int i = lo; i < hi; ++i) {
@@ -233,7 +245,7 @@ __device__ int2 block_exscan2(int32_t *a, int32_t *b, int N, int32_t *s_tmp) {
     rb += xb;
   }
   const int2 total = make_int2(s_tmp[nwaves - 1], s_tmp[32 + nwaves - 1]);
-  __syncthreads();
+  lds_barrier();
   return total;
 }
 
@@ -317,8 +329,15 @@ struct TokSmem {
   uint32_t db[kDW];                  // the token's department bitmap
 };
 
+// Per-token results handed to a plan in the same workgroup through LDS
+// (all null when the plan runs as its own kernel).
+struct PlanIn {
+  int32_t *ids, *dep, *nd;
+};
+
 template <int NS>
-__device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSmem &sm) {
+__device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSmem &sm,
+                          PlanIn lds = {nullptr, nullptr, nullptr}) {
   uint64_t *s_sel = sm.sel, *s_ord = sm.ord;
   int32_t *s_gs = sm.gs;
   uint32_t *s_db = sm.db;
@@ -540,6 +559,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
   const int d = sel ? my_id / E : 0;
   if (sel) {
     a.r.topk_ids[t * k + lane] = my_id;
+    if (lds.ids) lds.ids[t * k + lane] = my_id;
     a.r.topk_w[t * k + lane] = p;
     atomicOr(&s_db[d >> 5], 1u << (d & 31));
   }
@@ -563,16 +583,19 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
   if (first) {
     const int dpos = rank_below(s_db, d);
     a.r.tok_depts[t * k + dpos] = d;
+    if (lds.dep) lds.dep[t * k + dpos] = d;
     a.r.tok_dept_w[t * k + dpos] = P;
     if (a.plan) a.slot_w[(size_t)t * S + dpos] = slice ? P : 1.0f;
   }
   if (lane >= nd && lane < k) {
     a.r.tok_depts[t * k + lane] = -1;
+    if (lds.dep) lds.dep[t * k + lane] = -1;
     a.r.tok_dept_w[t * k + lane] = 0.f;
   }
   if (a.plan && exp_slots && sel) a.slot_w[(size_t)t * S + nd + lane] = p;
   if (lane == 0) {
     a.r.tok_ndept[t] = nd;
+    if (lds.nd) lds.nd[t] = nd;
     if (a.plan) {
       const int ns = nd + (exp_slots ? k : 0);
       if (a.d_se > 0) a.slot_w[(size_t)t * S + ns] = 1.0f;
@@ -607,8 +630,9 @@ struct PlanSmem {
   int32_t tmp[64];
 };
 
-// Every thread of the workgroup (BT threads) calls it.
-template <int BT>
+// Every thread of the workgroup (BT threads) calls it.  LDS_IN: the
+// per-token results are already in sm.ids, sm.dep and sm.nd.
+template <int BT, bool LDS_IN = false>
 __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
   constexpr int EPT = kMaxN / BT;   // experts per thread in the per-expert loops
   int32_t *s_ids = sm.ids, *s_dep = sm.dep, *s_scan = sm.scan, *s_nd = sm.nd, *s_tmp = sm.tmp;
@@ -623,18 +647,22 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
   const int S = a.max_slots;
   for (int i = tid; i < n * kTW; i += BT) s_etok[i] = 0;
   for (int i = tid; i < m * kTW; i += BT) s_dtok[i] = 0;
-  __syncthreads();
+  lds_barrier();
   for (int idx = tid; idx < T * k; idx += BT) {
     const int t = idx / k;
     const uint32_t bit = 1u << (t & 31);
-    const int e = a.r.topk_ids[idx], j = a.r.tok_depts[idx];
-    s_ids[idx] = e;
-    s_dep[idx] = j;
+    const int e = LDS_IN ? s_ids[idx] : a.r.topk_ids[idx];
+    const int j = LDS_IN ? s_dep[idx] : a.r.tok_depts[idx];
+    if (!LDS_IN) {
+      s_ids[idx] = e;
+      s_dep[idx] = j;
+    }
     atomicOr(&s_etok[e * kTW + (t >> 5)], bit);
     if (j >= 0) atomicOr(&s_dtok[j * kTW + (t >> 5)], bit);
   }
-  for (int t = tid; t < T; t += BT) s_nd[t] = a.r.tok_ndept[t];
-  __syncthreads();
+  if (!LDS_IN)
+    for (int t = tid; t < T; t += BT) s_nd[t] = a.r.tok_ndept[t];
+  lds_barrier();
 
   // counts
   int my_dc = 0, my_ec[EPT] = {};
@@ -654,7 +682,7 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       s_scan[m + e] = c | ((has_priv && c > 0) << 16);
     }
   }
-  __syncthreads();
+  lds_barrier();
   const int tot = block_exscan(s_scan, m + n, s_tmp);
   const int ndp = s_scan[m] & 0xffff, ud = s_scan[m] >> 16;
   const int nep = (tot & 0xffff) - ndp, ue = (tot >> 16) - ud;
@@ -736,7 +764,7 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
   }
   int tot_a = 0, tot_b = 0;
   if (multi) {
-    __syncthreads();   // the expert bitmaps are no longer read
+    lds_barrier();   // the expert bitmaps are no longer read
     if (tid < m) {
       s_ia[tid] = my_dc > 0 ? ia_d * groups(my_dc) : 0;
       s_ib[tid] = my_dc > 0 ? ib_d * groups(my_dc) : 0;
@@ -750,7 +778,7 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
         s_ib[m + e] = act ? ib_e * groups(my_ec[q]) : 0;
       }
     }
-    __syncthreads();
+    lds_barrier();
     const int2 tot = block_exscan2(s_ia, s_ib, m + n, s_tmp);
     tot_a = tot.x;
     tot_b = tot.y;
@@ -884,20 +912,49 @@ __global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
   plan_body<BT>(a, sm);
 }
 
-hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
-  const dim3 g(a.T), b(64);
-  switch (route_ns(a.n)) {
-    case 1: hipLaunchKernelGGL((route_token_kernel<1>), g, b, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((route_token_kernel<2>), g, b, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((route_token_kernel<4>), g, b, 0, s, a); break;
-    case 8: hipLaunchKernelGGL((route_token_kernel<8>), g, b, 0, s, a); break;
-    case 16: hipLaunchKernelGGL((route_token_kernel<16>), g, b, 0, s, a); break;
-    default: hipLaunchKernelGGL((route_token_kernel<32>), g, b, 0, s, a); break;
+// Batches of at most kFusedMaxT tokens route and plan in one workgroup: wave
+// t routes token t (one routing wave per SIMD) and leaves its results in LDS
+// as well, and the plan starts after a barrier that waits for LDS only (the
+// results' global stores complete in the background).  Larger batches route
+// in a workgroup per token, which spreads the routing over as many CUs.
+// Wider routers (more experts per lane) take fewer waves for the plan, which
+// leaves each wave more registers.
+constexpr int kFusedMaxT = 4;
+template <int NS>
+constexpr int fused_waves() { return NS <= 4 ? 16 : NS <= 16 ? 8 : 4; }
+
+template <int NS>
+__global__ __launch_bounds__(fused_waves<NS>() * 64) void route_plan_kernel(RouteArgs a) {
+  __shared__ TokSmem tsm[fused_waves<NS>()];
+  __shared__ PlanSmem psm;
+  const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
+  if (w < a.T) route_one<NS>(a, w, lane, tsm[w], PlanIn{psm.ids, psm.dep, psm.nd});
+  lds_barrier();
+  plan_body<fused_waves<NS>() * 64, true>(a, psm);
+}
+
+template <int NS>
+static hipError_t launch_route_ns(const RouteArgs &a, hipStream_t s) {
+  if (a.T <= kFusedMaxT) {
+    hipLaunchKernelGGL((route_plan_kernel<NS>), dim3(1), dim3(fused_waves<NS>() * 64), 0, s, a);
+    return hipGetLastError();
   }
+  hipLaunchKernelGGL((route_token_kernel<NS>), dim3(a.T), dim3(64), 0, s, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((plan_kernel<1024>), dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
+}
+
+hipError_t launch_route(const RouteArgs &a, hipStream_t s) {
+  switch (route_ns(a.n)) {
+    case 1: return launch_route_ns<1>(a, s);
+    case 2: return launch_route_ns<2>(a, s);
+    case 4: return launch_route_ns<4>(a, s);
+    case 8: return launch_route_ns<8>(a, s);
+    case 16: return launch_route_ns<16>(a, s);
+    default: return launch_route_ns<32>(a, s);
+  }
 }
 
 }  // namespace deamoe
