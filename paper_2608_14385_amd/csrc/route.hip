@@ -385,6 +385,20 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     }
   }
 
+  // departments of the lane's experts: one division, then stepped along the
+  // run (a division by the runtime E is a long instruction sequence)
+  int dep[NS];
+  {
+    int d = e0 / E, r = e0 - d * E;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      dep[s] = d;
+      const bool wrap = ++r == E;
+      r = wrap ? 0 : r;
+      d = wrap ? d + 1 : d;
+    }
+  }
+
   // group-limited top-k: keep the kdept departments with the largest maximum
   // logit (ties to the lower department id)
   uint64_t keep = ~0ull;
@@ -393,7 +407,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     wave_lds_sync();
 #pragma unroll
     for (int s = 0; s < NS; ++s)
-      if (e0 + s < n) atomicMax(&s_gs[(e0 + s) / E], ord_key(lv[s]));
+      if (e0 + s < n) atomicMax(&s_gs[dep[s]], ord_key(lv[s]));
     wave_lds_sync();
     const float gsv = lane < m ? ord_val(s_gs[lane]) : -INFINITY;
     keep = 0;
@@ -410,7 +424,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     const int e = e0 + s;
-    const bool ok = e < n && (a.kdept == 0 || ((keep >> ((e / E) & 63)) & 1));
+    const bool ok = e < n && (a.kdept == 0 || ((keep >> (dep[s] & 63)) & 1));
     key[s] = ok ? ord_u32(lv[s]) : 0u;
   }
   // Candidates.  theta, the k-th largest of the per-lane maxima, bounds the
@@ -511,7 +525,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
       for (int s = 0; s < NS; ++s) {
         const int e = e0 + s;
         const uint64_t c = ((uint64_t)key[s] << 32) | (uint32_t)~(uint32_t)e;
-        if (key[s] != 0u && !((cov >> ((e / E) & 63)) & 1) && c > best) best = c;
+        if (key[s] != 0u && !((cov >> (dep[s] & 63)) & 1) && c > best) best = c;
       }
       best = wave_max_u64(best);
       const uint64_t vm = __ballot(sel && mult >= 2);
