@@ -259,6 +259,22 @@ def test_factored_sigma(variant, sigma):
         check_case(case, tokens=sample_tokens(16, 2))
 
 
+@pytest.mark.parametrize("variant", ["fp8", "fp8_rmsnorm", "fp8_strict_t128"])
+def test_factored_fp8(variant):
+    """FACTORED form with e4m3 block-128 weights (all six expert matrices and
+    the shared expert), bf16 activations."""
+    base = P["tiny_factored"].layer.replace(w_dtype="fp8", act_dtype="bf16", n_experts=32,
+                                            n_depts=4, top_k=5, top_k_dept=2, score="sigmoid",
+                                            d_shared_expert=128)
+    if variant == "fp8":
+        case = Case(base, 13, seed=28)
+    elif variant == "fp8_rmsnorm":
+        case = Case(base.replace(sigma="rmsnorm"), 13, seed=29)
+    else:
+        case = Case(base.replace(dept_cover=1), 128, seed=30, max_tokens=128)
+    check_case(case, tokens=sample_tokens(case.T, 4) if case.T > 16 else None)
+
+
 def test_empty_batch_is_a_no_op():
     cfg = P["tiny_f32"].layer
     w = W.make_weights(cfg, 0, device="cuda")
