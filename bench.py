@@ -36,8 +36,8 @@ HBM_PEAK_GBPS = 8000.0
 # FETCH_SIZE and WRITE_SIZE passes scaled by what the same counters read for a
 # 1 GiB device copy (x2.0 and x1.0).  Valid only for the library sources they
 # were taken on: the digest below covers them, and a mismatch reports null.
-TRAFFIC_BYTES = 2341126880
-TRAFFIC_SOURCES_SHA256 = "bd3e7787c91d563cfd7188f34a4070444e2bfaa7268a434a392e85ac9a544a2c"
+TRAFFIC_BYTES = 2341127232
+TRAFFIC_SOURCES_SHA256 = "1a52edfc854bb7c37cac35fde59832efd88df47d2e7f6c2714350faa3b1f43dd"
 
 
 def library_sources_digest() -> str:
