@@ -130,8 +130,10 @@ def test_dsv3_fp8(T):
     check_case(case, tokens=sample_tokens(T))
 
 
-@pytest.mark.parametrize("T", [1, 16])
+@pytest.mark.parametrize("T", [1, 16, 64])
 def test_dsv3_factored(T):
+    """64 tokens: departments with more than one 32-token group (item prefixes
+    from block scans in the plan)."""
     case = Case(P["dsv3_factored"].layer, T, seed=80 + T)
     check_case(case, tokens=sample_tokens(T, 2))
 
@@ -170,7 +172,7 @@ def test_deterministic_and_route_only():
         assert np.array_equal(h1[k], h3[k]), k
 
 
-@pytest.mark.parametrize("T", [12, 40])
+@pytest.mark.parametrize("T", [3, 12, 40])
 @pytest.mark.parametrize("preset", ["tiny_f32", "7b_bf16", "dsv3_bf16", "dsv3_factored"])
 def test_route_ties(preset, T):
     """Coarse injected logits: many exact ties, including every logit equal
@@ -180,13 +182,14 @@ def test_route_ties(preset, T):
     cfg = P[preset].layer
     n = cfg.n_experts
     g = torch.Generator(device="cpu").manual_seed(5 + T)
-    u = torch.rand(T, n, generator=g)
+    u = torch.rand(max(T, 5), n, generator=g)
     rows = [torch.full((n,), 0.5),                                  # all equal
             torch.round(u[1] * 4) / 4,                              # five levels
             torch.round(u[2] * 64) / 64,                            # 65 levels
             torch.where(u[3] > 0.97, torch.tensor(2.0), u[3]),      # equal maxima
             torch.where(u[4] > 0.5, torch.tensor(0.0), torch.tensor(-0.0))]   # +0 and -0 tie
     rows += [torch.round(u[t] * (1 + t)) / (1 + t) for t in range(5, T)]
+    rows = rows[:T]   # up to four tokens route and plan in one workgroup
     logits = torch.stack(rows).to(torch.float32).contiguous()
     act = torch.float32 if cfg.act_dtype == "f32" else torch.bfloat16
     x = torch.zeros(T, cfg.hidden, dtype=act)
@@ -201,13 +204,15 @@ def test_route_ties(preset, T):
     compare_routing(rt.host(), ref, T, cfg.top_k)
 
 
+@pytest.mark.parametrize("T", [3, 40])
 @pytest.mark.parametrize("kind", ["ties", "gaussian"])
 @pytest.mark.parametrize("preset", ["dsv3_factored", "qwen3_factored", "base7b_factored"])
-def test_route_strict_coverage(preset, kind):
+def test_route_strict_coverage(preset, kind, T):
     """Strict department coverage (Sec. 3.4) on the Table 1 FACTORED shapes:
-    exactly top_k_dept departments per token, ids bit-exact with the oracle."""
+    exactly top_k_dept departments per token, ids bit-exact with the oracle
+    (3 tokens: the one-workgroup route and plan; 40: a workgroup per token)."""
     cfg = P[preset].layer.replace(dept_cover=1)
-    n, T = cfg.n_experts, 40
+    n = cfg.n_experts
     g = torch.Generator(device="cpu").manual_seed(17)
     u = torch.randn(T, n, generator=g)
     if kind == "ties":
