@@ -133,6 +133,19 @@ def _make_presets() -> dict:
                      renorm=True, sigma="silu", w_dtype="bf16", act_dtype="bf16")
     p["base7b_factored"] = Workload(b7, _vanilla(b7, "base7b_vanilla_256x384", 256, 8, 384),
                                     (1, 4, 16, 64))
+    # The DeepSeek-V2 and Kimi-K2 rows of Table 1.  DeepSeek-V2 keeps its own
+    # gate (softmax over all experts, top-k weights not renormalised); Kimi-K2
+    # follows DeepSeek-V3 (sigmoid, renormalised).
+    v2 = LayerConfig("dsv2_factored", hidden=5120, n_experts=512, n_depts=8, top_k=10,
+                     top_k_dept=5, d_shared=1536, form="factored", score="softmax",
+                     renorm=False, sigma="silu", w_dtype="bf16", act_dtype="bf16")
+    p["dsv2_factored"] = Workload(v2, _vanilla(v2, "dsv2_vanilla_160x1536", 160, 6, 1536),
+                                  (1, 4, 16, 64))
+    km = LayerConfig("kimik2_factored", hidden=7168, n_experts=1280, n_depts=16, top_k=10,
+                     top_k_dept=5, d_shared=2048, form="factored", score="sigmoid",
+                     renorm=True, sigma="silu", w_dtype="bf16", act_dtype="bf16")
+    p["kimik2_factored"] = Workload(km, _vanilla(km, "kimik2_vanilla_384x2048", 384, 8, 2048),
+                                    (1, 4, 16, 64))
     return p
 
 

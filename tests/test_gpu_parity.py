@@ -147,6 +147,23 @@ def test_table1_factored(preset, T):
     check_case(case, tokens=sample_tokens(T, 2))
 
 
+@pytest.mark.parametrize("preset", ["dsv2_factored", "kimik2_factored"])
+def test_table1_factored_more(preset):
+    """The DeepSeek-V2 (512 experts, softmax without renormalisation) and
+    Kimi-K2 (1280 experts in 16 departments) rows of Table 1, one weight draw
+    at 1 and 16 tokens."""
+    cfg = P[preset].layer
+    w = W.make_weights(cfg, 120, device="cuda", gate_exact=True)
+    hw = None   # one host copy of the weights for both batches
+    for T in (1, 16):
+        case = Case(cfg, T, seed=120 + T, weights=w)
+        case._host = hw
+        check_case(case, tokens=sample_tokens(T, 2))
+        hw = case._host
+    del w, hw, case
+    torch.cuda.empty_cache()
+
+
 def test_dsv3_baseline():
     case = Case(P["dsv3_bf16"].baseline, 16, seed=90)
     check_case(case, tokens=sample_tokens(16, 2), baseline=True)
@@ -173,7 +190,8 @@ def test_deterministic_and_route_only():
 
 
 @pytest.mark.parametrize("T", [3, 12, 40])
-@pytest.mark.parametrize("preset", ["tiny_f32", "7b_bf16", "dsv3_bf16", "dsv3_factored"])
+@pytest.mark.parametrize("preset", ["tiny_f32", "7b_bf16", "dsv3_bf16", "dsv3_factored",
+                                    "dsv2_factored", "kimik2_factored"])
 def test_route_ties(preset, T):
     """Coarse injected logits: many exact ties, including every logit equal
     (more candidates than one per lane, so the exact selection path runs), a
