@@ -257,8 +257,19 @@ __device__ inline void wave_lds_sync() {
 
 constexpr int kMaxKC = 16;   // router chunks (host caps the split)
 
+// Global-address-space view of a pointer.  The plan reads its pointers from
+// an LDS copy of the argument block, which leaves the compiler without the
+// knowledge that they address global memory (stores through them would
+// become flat stores, which also hold up every later LDS wait).
+template <class T>
+using gmem = __attribute__((address_space(1))) T;
+template <class T>
+__device__ inline gmem<T> *glob(T *p) {
+  return reinterpret_cast<gmem<T> *>(reinterpret_cast<uintptr_t>(p));
+}
+
 // Fill one unit of a stage table field by field (no temporary struct).
-__device__ inline void put_unit(GemmUnit *U, const void *w0, const void *w1, const float *s0,
+__device__ inline void put_unit(gmem<GemmUnit> *U, const void *w0, const void *w1, const float *s0,
                                 const float *s1, const void *in0, const void *in1,
                                 const int32_t *idx, void *out0, void *out1, int R, int K, int ldin,
                                 int ldout, int ntok, int tile_begin, int epi, int out_f32,
@@ -647,7 +658,7 @@ struct PlanSmem {
 // Every thread of the workgroup (BT threads) calls it.  LDS_IN: the
 // per-token results are already in sm.ids, sm.dep and sm.nd.
 template <int BT, bool LDS_IN = false>
-__device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
+__device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, PlanSmem &sm) {
   constexpr int EPT = kMaxN / BT;   // experts per thread in the per-expert loops
   int32_t *s_ids = sm.ids, *s_dep = sm.dep, *s_scan = sm.scan, *s_nd = sm.nd, *s_tmp = sm.tmp;
   uint32_t *s_etok = sm.etok, *s_dtok = sm.dtok;
@@ -659,14 +670,20 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
   const bool has_priv = a.plan == PLAN_FACTORED || a.d_p > 0;
   const bool has_se = a.d_se > 0;
   const int S = a.max_slots;
+  gmem<int32_t> *dept_count = glob(a.r.dept_count), *exp_count = glob(a.r.exp_count);
+  gmem<int32_t> *dept_offset = glob(a.r.dept_offset), *exp_offset = glob(a.r.exp_offset);
+  gmem<int32_t> *dept_tokens = glob(a.r.dept_tokens), *exp_tokens = glob(a.r.exp_tokens);
+  gmem<int32_t> *slot_pair = glob(a.slot_pair), *tok_exp_pair = glob(a.tok_exp_pair);
+  gmem<int32_t> *exp_src = glob(a.exp_src), *pair_dept = glob(a.pair_dept);
+  gmem<PlanCounts> *counts = glob(a.counts);
   for (int i = tid; i < n * kTW; i += BT) s_etok[i] = 0;
   for (int i = tid; i < m * kTW; i += BT) s_dtok[i] = 0;
   lds_barrier();
   for (int idx = tid; idx < T * k; idx += BT) {
     const int t = idx / k;
     const uint32_t bit = 1u << (t & 31);
-    const int e = LDS_IN ? s_ids[idx] : a.r.topk_ids[idx];
-    const int j = LDS_IN ? s_dep[idx] : a.r.tok_depts[idx];
+    const int e = LDS_IN ? s_ids[idx] : glob(a.r.topk_ids)[idx];
+    const int j = LDS_IN ? s_dep[idx] : glob(a.r.tok_depts)[idx];
     if (!LDS_IN) {
       s_ids[idx] = e;
       s_dep[idx] = j;
@@ -675,14 +692,14 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
     if (j >= 0) atomicOr(&s_dtok[j * kTW + (t >> 5)], bit);
   }
   if (!LDS_IN)
-    for (int t = tid; t < T; t += BT) s_nd[t] = a.r.tok_ndept[t];
+    for (int t = tid; t < T; t += BT) s_nd[t] = glob(a.r.tok_ndept)[t];
   lds_barrier();
 
   // counts
   int my_dc = 0, my_ec[EPT] = {};
   if (tid < m) {
     for (int w = 0; w < tw; ++w) my_dc += __popc(s_dtok[tid * kTW + w]);
-    a.r.dept_count[tid] = my_dc;
+    dept_count[tid] = my_dc;
     s_scan[tid] = my_dc | ((my_dc > 0) << 16);
   }
 #pragma unroll
@@ -692,7 +709,7 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       int c = 0;
       for (int w = 0; w < tw; ++w) c += __popc(s_etok[e * kTW + w]);
       my_ec[q] = c;
-      a.r.exp_count[e] = c;
+      exp_count[e] = c;
       s_scan[m + e] = c | ((has_priv && c > 0) << 16);
     }
   }
@@ -703,11 +720,11 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
   const int nep_priv = has_priv ? nep : 0;
   auto doff = [&](int j) { return s_scan[j] & 0xffff; };
   auto eoff = [&](int e) { return (s_scan[m + e] & 0xffff) - ndp; };
-  if (tid < m) a.r.dept_offset[tid] = doff(tid);
-  for (int e = tid; e < n; e += BT) a.r.exp_offset[e] = eoff(e);
+  if (tid < m) dept_offset[tid] = doff(tid);
+  for (int e = tid; e < n; e += BT) exp_offset[e] = eoff(e);
   if (tid == 0) {
-    a.r.dept_offset[m] = ndp;
-    a.r.exp_offset[n] = nep;
+    dept_offset[m] = ndp;
+    exp_offset[n] = nep;
   }
   // every (token, rank) pair places itself: the expert of that rank and, for
   // ranks below the token's department count, the department of that slot
@@ -715,27 +732,27 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
     const int t = idx / k, q = idx - t * k;
     const int e = s_ids[idx];
     const int pe = eoff(e) + rank_below(s_etok + e * kTW, t);
-    a.r.exp_tokens[pe] = t;
+    exp_tokens[pe] = t;
     if (a.plan) {
-      a.tok_exp_pair[idx] = pe;
-      if (exp_slots) a.slot_pair[(size_t)t * S + s_nd[t] + q] = ndp + pe;
+      tok_exp_pair[idx] = pe;
+      if (exp_slots) slot_pair[(size_t)t * S + s_nd[t] + q] = ndp + pe;
       if (a.plan == PLAN_FACTORED) {
         const int j = e / E;
-        a.exp_src[pe] = doff(j) + rank_below(s_dtok + j * kTW, t);
+        exp_src[pe] = doff(j) + rank_below(s_dtok + j * kTW, t);
       }
     }
     const int j = s_dep[idx];
     if (j >= 0) {
       const int pd = doff(j) + rank_below(s_dtok + j * kTW, t);
-      a.r.dept_tokens[pd] = t;
-      if (a.plan) a.slot_pair[(size_t)t * S + q] = pd;
-      if (a.plan == PLAN_FACTORED) a.pair_dept[pd] = j;
+      dept_tokens[pd] = t;
+      if (a.plan) slot_pair[(size_t)t * S + q] = pd;
+      if (a.plan == PLAN_FACTORED) pair_dept[pd] = j;
     }
   }
   if (!a.plan) return;
   if (has_se)
     for (int t = tid; t < T; t += BT)
-      a.slot_pair[(size_t)t * S + s_nd[t] + (exp_slots ? k : 0)] = ndp + (slice ? nep_priv : 0) + t;
+      slot_pair[(size_t)t * S + s_nd[t] + (exp_slots ? k : 0)] = ndp + (slice ? nep_priv : 0) + t;
 
   // unit tables: unit index of an active department / expert = number of
   // active ones before it.  A unit's work items are its row-tile items times
@@ -815,10 +832,10 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       const int j = tid, u = s_scan[j] >> 16, off = doff(j);
       const int32_t *idx = a.r.dept_tokens + off;
       char *ao = static_cast<char *>(a.abuf_dept) + (size_t)off * a.d_s * ab;
-      put_unit(&a.units[0][u], wptr(W.dept_gate, j, a.d_s, a.h), wptr(W.dept_up, j, a.d_s, a.h),
+      put_unit(glob(a.units[0]) + u, wptr(W.dept_gate, j, a.d_s, a.h), wptr(W.dept_up, j, a.d_s, a.h),
                sptr(W.scale[0], j, a.d_s, a.h), sptr(W.scale[1], j, a.d_s, a.h), x, x, idx, ao,
                nullptr, a.d_s, a.h, a.h, a.d_s, my_dc, dbeg_a(j, u), EPI_SWIGLU, a.act_f32);
-      put_unit(&a.units[1][u], wptr(W.dept_down, j, a.h, a.d_s), nullptr,
+      put_unit(glob(a.units[1]) + u, wptr(W.dept_down, j, a.h, a.d_s), nullptr,
                sptr(W.scale[2], j, a.h, a.d_s), nullptr, ao, ao, nullptr,
                a.partial + (size_t)off * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, my_dc,
                dbeg_b(j, u), EPI_STORE, 1, gd);
@@ -830,11 +847,11 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       const int ui = (s_scan[m + e] >> 16) - ud, u = ud + ui, off = eoff(e);
       const int32_t *idx = a.r.exp_tokens + off;
       char *ao = static_cast<char *>(a.abuf_exp) + (size_t)off * a.d_p * ab;
-      put_unit(&a.units[0][u], wptr(W.priv_gate, e, a.d_p, a.h), wptr(W.priv_up, e, a.d_p, a.h),
+      put_unit(glob(a.units[0]) + u, wptr(W.priv_gate, e, a.d_p, a.h), wptr(W.priv_up, e, a.d_p, a.h),
                sptr(W.scale[3], e, a.d_p, a.h), sptr(W.scale[4], e, a.d_p, a.h), x, x, idx, ao,
                nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q], ebeg_a(e, ui), EPI_SWIGLU,
                a.act_f32);
-      put_unit(&a.units[1][u], wptr(W.priv_down, e, a.h, a.d_p), nullptr,
+      put_unit(glob(a.units[1]) + u, wptr(W.priv_down, e, a.h, a.d_p), nullptr,
                sptr(W.scale[5], e, a.h, a.d_p), nullptr, ao, ao, nullptr,
                a.partial + (size_t)(ndp + off) * a.h, nullptr, a.h, a.d_p, a.d_p, a.h, my_ec[q],
                ebeg_b(e, ui), EPI_STORE, 1, gp);
@@ -842,20 +859,20 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
     if (tid == 0) {
       int units = ud + ue, items_a = tot_a, items_b = tot_b;
       if (has_se) {
-        put_unit(&a.units[0][units], W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
+        put_unit(glob(a.units[0]) + units, W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
                  a.h, a.d_se, T, items_a, EPI_SWIGLU, a.act_f32);
-        put_unit(&a.units[1][units], W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se), nullptr,
+        put_unit(glob(a.units[1]) + units, W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se), nullptr,
                  a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)(ndp + nep_priv) * a.h,
                  nullptr, a.h, a.d_se, a.d_se, a.h, T, items_b, EPI_STORE, 1, gse);
         items_a += (a.d_se + kTile - 1) / kTile * groups(T);
         items_b += bse * groups(T);
         ++units;
       }
-      a.counts->stage[0][0] = units;
-      a.counts->stage[0][1] = items_a;
-      a.counts->stage[1][0] = units;
-      a.counts->stage[1][1] = items_b;
+      counts->stage[0][0] = units;
+      counts->stage[0][1] = items_a;
+      counts->stage[1][0] = units;
+      counts->stage[1][1] = items_b;
     }
   } else {  // PLAN_FACTORED
     const int d = a.d_s;
@@ -868,10 +885,10 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       char *go = static_cast<char *>(a.gbuf) + (size_t)off * d * ab;
       char *uo = static_cast<char *>(a.ubuf) + (size_t)off * d * ab;
       char *zs = static_cast<char *>(a.zsbuf) + (size_t)off * d * ab;
-      put_unit(&a.units[0][u], wptr(W.dept_gate, j, d, a.h), wptr(W.dept_up, j, d, a.h),
+      put_unit(glob(a.units[0]) + u, wptr(W.dept_gate, j, d, a.h), wptr(W.dept_up, j, d, a.h),
                sptr(W.scale[0], j, d, a.h), sptr(W.scale[1], j, d, a.h), x, x, idx, go, uo, d,
                a.h, a.h, d, my_dc, dbeg_a(j, u), EPI_SIGMA2, a.act_f32);
-      put_unit(&a.units[3][u], wptr(W.dept_down, j, a.h, d), nullptr, sptr(W.scale[2], j, a.h, d),
+      put_unit(glob(a.units[3]) + u, wptr(W.dept_down, j, a.h, d), nullptr, sptr(W.scale[2], j, a.h, d),
                nullptr, zs, zs, nullptr, a.partial + (size_t)off * a.h, nullptr, a.h, d, d,
                a.h, my_dc, dbeg_b(j, u), EPI_STORE, 1, gd);
     }
@@ -881,21 +898,21 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
       if (e >= n || my_ec[q] == 0) continue;
       const int u = (s_scan[m + e] >> 16) - ud, off = eoff(e);
       char *yo = static_cast<char *>(a.ybuf) + (size_t)off * d * ab;
-      put_unit(&a.units[1][u], wptr(W.priv_gate, e, d, d), wptr(W.priv_up, e, d, d),
+      put_unit(glob(a.units[1]) + u, wptr(W.priv_gate, e, d, d), wptr(W.priv_up, e, d, d),
                sptr(W.scale[3], e, d, d), sptr(W.scale[4], e, d, d), a.gbuf, a.ubuf,
                a.exp_src + off, yo, nullptr, d, d, d, d, my_ec[q], ebeg_a(e, u) - dept_a,
                EPI_SWIGLU, a.act_f32);
-      put_unit(&a.units[2][u], wptr(W.priv_down, e, d, d), nullptr, sptr(W.scale[5], e, d, d),
+      put_unit(glob(a.units[2]) + u, wptr(W.priv_down, e, d, d), nullptr, sptr(W.scale[5], e, d, d),
                nullptr, yo, yo, nullptr, a.zbuf + (size_t)off * d, nullptr, d, d, d, d,
                my_ec[q], ebeg_b(e, u) - dept_b, EPI_SIGMA, 1, g2);
     }
     if (tid == 0) {
       int units0 = ud, items0 = dept_a, units3 = ud, items3 = dept_b;
       if (has_se) {
-        put_unit(&a.units[0][units0], W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
+        put_unit(glob(a.units[0]) + units0, W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
                  a.h, a.d_se, T, items0, EPI_SWIGLU, a.act_f32);
-        put_unit(&a.units[3][units3], W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
+        put_unit(glob(a.units[3]) + units3, W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
                  nullptr, a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)ndp * a.h, nullptr,
                  a.h, a.d_se, a.d_se, a.h, T, items3, EPI_STORE, 1, gse);
         ++units0;
@@ -903,27 +920,42 @@ __device__ void plan_body(const RouteArgs &a, PlanSmem &sm) {
         ++units3;
         items3 += bse * groups(T);
       }
-      a.counts->stage[0][0] = units0;
-      a.counts->stage[0][1] = items0;
-      a.counts->stage[1][0] = ue;
-      a.counts->stage[1][1] = tot_a - dept_a;
-      a.counts->stage[2][0] = ue;
-      a.counts->stage[2][1] = tot_b - dept_b;
-      a.counts->stage[3][0] = units3;
-      a.counts->stage[3][1] = items3;
+      counts->stage[0][0] = units0;
+      counts->stage[0][1] = items0;
+      counts->stage[1][0] = ue;
+      counts->stage[1][1] = tot_a - dept_a;
+      counts->stage[2][0] = ue;
+      counts->stage[2][1] = tot_b - dept_b;
+      counts->stage[3][0] = units3;
+      counts->stage[3][1] = items3;
     }
   }
   if (tid == 0) {
-    a.counts->n_dept_pairs = ndp;
-    a.counts->n_exp_pairs = nep_priv;
-    a.counts->n_pairs = ndp + (slice ? nep_priv : 0) + (has_se ? T : 0);
+    counts->n_dept_pairs = ndp;
+    counts->n_exp_pairs = nep_priv;
+    counts->n_pairs = ndp + (slice ? nep_priv : 0) + (has_se ? T : 0);
   }
+}
+
+// The argument block copied to LDS by the first threads of the workgroup
+// (visible after the next barrier): the plan then loads each pointer where it
+// uses it instead of holding all of them in scalar registers, which spilled.
+template <int BT>
+__device__ inline void args_to_lds(const RouteArgs &a, RouteArgs &sa) {
+  static_assert(sizeof(RouteArgs) % 4 == 0 && sizeof(RouteArgs) / 4 <= BT, "argument copy");
+  const int tid = threadIdx.x;
+  if (tid < (int)(sizeof(RouteArgs) / 4))
+    __builtin_memcpy(reinterpret_cast<char *>(&sa) + 4 * tid,
+                     reinterpret_cast<const char *>(&a) + 4 * tid, 4);
 }
 
 template <int BT>
 __global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
   __shared__ PlanSmem sm;
-  plan_body<BT>(a, sm);
+  __shared__ RouteArgs sa;
+  args_to_lds<BT>(a, sa);
+  lds_barrier();
+  plan_body<BT>(sa, sm);
 }
 
 // Batches of at most kFusedMaxT tokens route and plan in one workgroup: wave
@@ -941,10 +973,12 @@ template <int NS>
 __global__ __launch_bounds__(fused_waves<NS>() * 64) void route_plan_kernel(RouteArgs a) {
   __shared__ TokSmem tsm[fused_waves<NS>()];
   __shared__ PlanSmem psm;
+  __shared__ RouteArgs sa;
   const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
+  args_to_lds<fused_waves<NS>() * 64>(a, sa);
   if (w < a.T) route_one<NS>(a, w, lane, tsm[w], PlanIn{psm.ids, psm.dep, psm.nd});
   lds_barrier();
-  plan_body<fused_waves<NS>() * 64, true>(a, psm);
+  plan_body<fused_waves<NS>() * 64, true>(sa, psm);
 }
 
 template <int NS>

@@ -124,10 +124,33 @@ def test_dsv3_skew_gumbel():
     check_case(case, tokens=sample_tokens(96))
 
 
-@pytest.mark.parametrize("T", [1, 32])
+@pytest.mark.parametrize("T", [1, 16, 32])
 def test_dsv3_fp8(T):
     case = Case(P["dsv3_fp8"].layer, T, seed=70 + T)
     check_case(case, tokens=sample_tokens(T))
+
+
+@pytest.mark.parametrize("variant", ["wide_t5", "wide_t40_se", "wide_factored", "narrow",
+                                     "wide_baseline"])
+def test_fp8_step_widths(variant):
+    """e4m3 block-128 weights on small layers, every output checked.  When
+    every contraction is a multiple of 256 the weights stream two scale blocks
+    per K step (wide); otherwise one (narrow, a 128-wide private slice)."""
+    base = small(hidden=512, d_shared=512, d_private=256, score="sigmoid", w_dtype="fp8",
+                 act_dtype="bf16", n_experts=16, n_depts=4, top_k=3)
+    baseline = False
+    if variant == "wide_t5":
+        case = Case(base, 5, seed=31)
+    elif variant == "wide_t40_se":
+        case = Case(base.replace(d_shared_expert=256), 40, seed=32, max_tokens=64)
+    elif variant == "wide_factored":
+        case = Case(base.replace(form="factored", d_shared=256, d_private=0), 21, seed=33)
+    elif variant == "narrow":
+        case = Case(base.replace(d_private=128), 21, seed=34)
+    else:
+        cfg = base.replace(name="small_baseline", n_depts=16, d_shared=768, d_private=0)
+        case, baseline = Case(cfg, 17, seed=35), True
+    check_case(case, baseline=baseline)
 
 
 @pytest.mark.parametrize("T", [1, 16, 64])
