@@ -130,22 +130,23 @@ def test_dsv3_fp8(T):
     check_case(case, tokens=sample_tokens(T))
 
 
-@pytest.mark.parametrize("variant", ["wide_t5", "wide_t40_se", "wide_factored", "narrow",
-                                     "wide_baseline"])
-def test_fp8_step_widths(variant):
-    """e4m3 block-128 weights on small layers, every output checked.  When
-    every contraction is a multiple of 256 the weights stream two scale blocks
-    per K step (wide); otherwise one (narrow, a 128-wide private slice)."""
+@pytest.mark.parametrize("variant", ["slice_t5", "slice_t40_se", "factored", "private_128",
+                                     "baseline"])
+def test_fp8_small(variant):
+    """e4m3 block-128 weights on small layers, every output checked: several
+    scale blocks along each contraction and across the rows, a shared expert
+    at two token groups, the FACTORED form, a private slice of a single scale
+    block, and the vanilla layer."""
     base = small(hidden=512, d_shared=512, d_private=256, score="sigmoid", w_dtype="fp8",
                  act_dtype="bf16", n_experts=16, n_depts=4, top_k=3)
     baseline = False
-    if variant == "wide_t5":
+    if variant == "slice_t5":
         case = Case(base, 5, seed=31)
-    elif variant == "wide_t40_se":
+    elif variant == "slice_t40_se":
         case = Case(base.replace(d_shared_expert=256), 40, seed=32, max_tokens=64)
-    elif variant == "wide_factored":
+    elif variant == "factored":
         case = Case(base.replace(form="factored", d_shared=256, d_private=0), 21, seed=33)
-    elif variant == "narrow":
+    elif variant == "private_128":
         case = Case(base.replace(d_private=128), 21, seed=34)
     else:
         cfg = base.replace(name="small_baseline", n_depts=16, d_shared=768, d_private=0)
