@@ -78,6 +78,9 @@ extern "C" {
 #define DEAMOE_MAX_TOKENS 128
 #define DEAMOE_MAX_EXPERTS 2048
 #define DEAMOE_MAX_TOPK 32
+/* fp8 weights: every contraction length (hidden, d_shared, d_private,
+ * d_shared_expert) is at most this many columns (64 scale blocks) */
+#define DEAMOE_MAX_FP8_K 8192
 
 typedef struct {
   int32_t hidden;           /* h                                                        */

@@ -137,6 +137,11 @@ int validate_config(const deamoe_config *c) {
   if (c->hidden % ks || c->d_shared % ks) return DEAMOE_ERR_UNSUPPORTED;
   if (c->form == DEAMOE_FORM_SLICE && c->d_private % ks) return DEAMOE_ERR_UNSUPPORTED;
   if (c->d_shared_expert % ks) return DEAMOE_ERR_UNSUPPORTED;
+  // a work item holds its fp8 block scales as one 64-entry window
+  if (c->w_dtype == DEAMOE_FP8_E4M3_B128 &&
+      (c->hidden > DEAMOE_MAX_FP8_K || c->d_shared > DEAMOE_MAX_FP8_K ||
+       c->d_private > DEAMOE_MAX_FP8_K || c->d_shared_expert > DEAMOE_MAX_FP8_K))
+    return DEAMOE_ERR_UNSUPPORTED;
   return DEAMOE_OK;
 }
 

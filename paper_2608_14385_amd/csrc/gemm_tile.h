@@ -72,9 +72,13 @@ __device__ inline bf16x8 fp8x8_to_bf16(uint32_t lo, uint32_t hi) {
 }
 
 typedef __attribute__((address_space(1))) const u32x4 gvec;
+typedef __attribute__((address_space(1))) const float gfloat;
 
 __device__ inline const gvec *gptr(const void *p) {
   return reinterpret_cast<const gvec *>(reinterpret_cast<uintptr_t>(p));
+}
+__device__ inline const gfloat *gfptr(const float *p) {
+  return reinterpret_cast<const gfloat *>(reinterpret_cast<uintptr_t>(p));
 }
 
 // Token-operand row of token i of a unit.
@@ -190,12 +194,27 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
                         : NW == 2 ? static_cast<const char *>(U.w1) + lchunk * 16 : w0;
   const int rmax = R - 1 - (PAIR ? kTile : 0);   // last row the first matrix may read
   const char *dummy = bp0[0] + (lane & 15) * 16;
+  // fp8 block scales.  The scale rows of this item's tiles are read once, as a
+  // window of 64 entries of the [R/128, K/128] table starting at the first
+  // tile's scale row: lane l holds entry l.  A K step then takes its scale
+  // with one lane read instead of a load.  The window covers the item: a
+  // single tile lies in one scale row (TR divides 128) and K / 128 <= 64; a
+  // multi-tile item spans at most 32768 / K rows with K <= 1024, at most
+  // 2 + K / 64 <= 18 entries.
   const int sblocks = U.K / 128;
+  float scw[NW];
+  const int srow0 = (rt0 * TR) / 128;
+  if constexpr (WT == WT_FP8) {
+    const int base = srow0 * sblocks, nsc = ((R + 127) / 128) * sblocks;
+    const int e = base + lane < nsc ? base + lane : base;
+    scw[0] = gfptr(U.s0)[e];
+    if constexpr (NW == 2) scw[1] = gfptr(PAIR ? U.s0 : U.s1)[e];
+  }
   u32x4 G[NB][NW][LD::NQ];
   u32x4 B[NB][NTT][BV];
-  float SC[NB][NW];
+  int SC[NB];   // fp8: window entry of the group's scales
   // issue the load group of virtual step v (tile v / nloc, K step kp + (v % nloc) * ks)
-  auto issue = [&](u32x4(&Gb)[NW][LD::NQ], u32x4(&Bb)[NTT][BV], float (&sc)[NW], int v) {
+  auto issue = [&](u32x4(&Gb)[NW][LD::NQ], u32x4(&Bb)[NTT][BV], int &sc, int v) {
     const bool ok = v < total;
     const int sub = ok ? v / nloc : 0;
     const int kstep = ok ? kp + (v - sub * nloc) * ks : 0;
@@ -208,11 +227,8 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
         Gb[n][q] = __builtin_nontemporal_load(gptr(ok ? (n ? w1 : w0) + woff : dummy));
     }
     load_b<WT, NTT, SPLIT>(Bb, bp0, bp1, ntt, (size_t)kstep * ASEG, g);
-    if constexpr (WT == WT_FP8) {
-      const int srow = ((rt0 + sub) * TR) / 128;   // a row pair lies in one scale block
-      sc[0] = U.s0[srow * sblocks + kstep];
-      if constexpr (NW == 2) sc[1] = (PAIR ? U.s0 : U.s1)[srow * sblocks + kstep];
-    }
+    if constexpr (WT == WT_FP8)   // a row pair lies in one scale row
+      sc = uniform((((rt0 + sub) * TR) / 128 - srow0) * sblocks + kstep);
   };
   // rows of the staged step in the matrix-core operand layout
   auto stage = [&](const u32x4(&Gb)[NW][LD::NQ], u32x4(&a)[NW][4]) {
@@ -247,7 +263,13 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
       __builtin_amdgcn_sched_barrier(0);
       u32x4 a[NW][4];
       stage(G[q], a);
-      step_mma<WT, NW, NTT, SPLIT>(a, B[q], ntt, SC[q], acc);
+      float sc[NW];
+      if constexpr (WT == WT_FP8) {
+#pragma unroll
+        for (int n = 0; n < NW; ++n)
+          sc[n] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scw[n]), SC[q]));
+      }
+      step_mma<WT, NW, NTT, SPLIT>(a, B[q], ntt, sc, acc);
       __builtin_amdgcn_sched_barrier(0);
       ++v;
       if (nsub > 1 && v % nloc == 0) {   // a tile of a multi-tile work item is complete

@@ -76,6 +76,10 @@ def ws_status(c):
     (dict(top_k_dept=9, n_depts=32, top_k=8, dept_cover=1), D.ERR_INVALID),   # k < k_dept
     (dict(sigma="gelu"), D.OK),
     (dict(sigma="rmsnorm"), D.OK),
+    (dict(w_dtype="fp8", hidden=8192), D.OK),
+    (dict(w_dtype="fp8", hidden=8192 + 128), D.ERR_UNSUPPORTED),   # more than 64 fp8 scale blocks
+    (dict(w_dtype="fp8", d_shared=8192 + 128), D.ERR_UNSUPPORTED),
+    (dict(hidden=8192 + 128), D.OK),                                # bf16 has no such limit
 ])
 def test_config_validation(mut, expect):
     if mut == dict(top_k_dept=1):
