@@ -218,11 +218,12 @@ class LayerRun:
         torch.cuda.synchronize()
         return a.elapsed_time(b) / (reps * per)
 
-    def time_stages(self, hip: Hip, steps: int) -> list:
+    def time_stages(self, hip: Hip, steps: int, n_ev: int | None = None) -> list:
         """Per-kernel durations (ms) from HIP events recorded between the
         kernels on the launch stream; returns one list of durations per step."""
         torch = self.torch
-        n_ev = 6 if self.cfg.form == "slice" else 9
+        if n_ev is None:
+            n_ev = self.D.deamoe_trace_points(self.c, self.T)
         evs = [[hip.event() for _ in range(n_ev)] for _ in range(steps)]
         torch.cuda.synchronize()
         for i in range(steps):
@@ -320,8 +321,10 @@ def multi_layer(cfg, base_cfg, L: int, T: int, reps: int) -> dict:
     return out
 
 
-def stage_names(form: str) -> list:
+def stage_names(form: str, n_stages: int) -> list:
     if form == "slice":
+        if n_stages == 4:   # down projections and combine in one kernel
+            return ["router_gemv", "route_plan", "gate_up", "down_combine"]
         return ["router_gemv", "route_plan", "gate_up", "down", "combine"]
     return ["router_gemv", "route_plan", "dept_gate_up", "priv_gate_up", "priv_down", "z_collect",
             "dept_down", "combine"]
@@ -493,7 +496,7 @@ def main():
     # per-kernel durations (HIP events on the launch stream, same region shape)
     if not args.no_stages:
         stages = run.time_stages(hip, args.steps)
-        names = stage_names(cfg.form)
+        names = stage_names(cfg.form, len(stages[0]))
         mean = np.mean(np.asarray(stages), axis=0)
         result["kernels_us"] = {n: round(float(v) * 1e3, 2) for n, v in zip(names, mean)}
         dom = names.index("gate_up" if cfg.form == "slice" else "dept_gate_up")

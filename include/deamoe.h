@@ -179,14 +179,21 @@ int deamoe_layer_forward(const deamoe_config *cfg, int32_t T, const void *x,
 /* The same with caller-created hipEvent_t handles recorded on `stream` at the
  * stage boundaries, for timing: events[0] before the router, then one after
  * each launched kernel in order (SLICE: router GEMV, route, gate/up, down,
- * combine; FACTORED: router GEMV, route, department gate/up, private gate/up,
+ * combine, where batches of at most 16 tokens run down and combine as one
+ * kernel; FACTORED: router GEMV, route, department gate/up, private gate/up,
  * private down, Z collect, department down, combine).  n_events may be
- * smaller than that count; NULL / 0 records nothing. */
+ * smaller than that count; NULL / 0 records nothing.  With injected logits
+ * the router GEMV is not launched and has no boundary. */
 int deamoe_layer_forward_traced(const deamoe_config *cfg, int32_t T, const void *x,
                                 const deamoe_weights *w, const float *logits_in,
                                 const float *router_bias, deamoe_routing *routing_out, void *y,
                                 void *ws, size_t ws_bytes, void *stream, void *const *events,
                                 int32_t n_events);
+
+/* Host: the number of events deamoe_layer_forward_traced records for a batch
+ * of T tokens with computed logits (1 + one per stage listed above).  Returns
+ * DEAMOE_ERR_INVALID for a NULL pointer, T < 1 or T > max_tokens. */
+int deamoe_trace_points(const deamoe_config *cfg, int32_t T, int32_t *n_events);
 
 /* Vanilla MoE of Eq. 1-3 at the same shape, the comparator for speedups:
  * cfg must describe one expert per department (n_depts == n_experts), no

@@ -44,6 +44,7 @@ struct Layout {
       dept_offset, dept_tokens, exp_count, exp_offset, exp_tokens;
   size_t counts, units[kMaxStages], slot_pair, slot_w, nslot, tok_exp_pair, exp_src, pair_dept;
   size_t abuf_dept, abuf_exp, abuf_se, gbuf, ubuf, ybuf, zbuf, zsbuf, partial;
+  size_t wdense, cunits;   // fused SLICE down stage
   size_t total;
   int kc, max_units, max_dept_pairs, max_exp_pairs;
 };
@@ -93,7 +94,12 @@ Layout make_layout(const deamoe_config &c) {
     L.abuf_exp = take(epairs * dp * ab);
     L.gbuf = L.ubuf = L.ybuf = L.zbuf = L.zsbuf = 0;
     L.partial = take((dpairs + (dp ? epairs : 0) + (dse ? T : 0)) * h * 4);
+    // fused down stage, batches of at most 16 tokens: routing weights per
+    // unit and token, the unit table
+    L.wdense = take((m + n + 1) * kTile * 4);
+    L.cunits = take((size_t)kMaxChainUnits * sizeof(ChainUnit));
   } else {
+    L.wdense = L.cunits = 0;
     L.abuf_dept = L.abuf_exp = 0;
     L.gbuf = take(dpairs * ds * ab);
     L.ubuf = take(dpairs * ds * ab);
@@ -187,6 +193,25 @@ int down_ks_of(const deamoe_config &c, int T) {
 }
 
 
+// Down projections and combine fused into one kernel (SLICE form): batches of
+// at most 16 tokens whose active units fit the kernel's unit table.  Its grid
+// is one workgroup per 32 rows of y; below kChainMinTiles of them (a hidden
+// size under 4096) it is used up to 4 tokens only, where the separate down
+// stage has too few work items to do better (measured on the 2048-wide layer).
+#ifndef DEAMOE_CHAIN
+#define DEAMOE_CHAIN 1
+#endif
+constexpr int kChainMinTiles = 128;
+bool use_chain(const deamoe_config &c, int T) {
+  if (!DEAMOE_CHAIN || c.form != DEAMOE_FORM_SLICE || T > kTile) return false;
+  if (T > 4 && c.hidden / (2 * kTile) < kChainMinTiles) return false;
+  const int dk = std::min(c.top_k_dept > 0 ? c.top_k_dept : c.top_k, std::min(c.top_k, c.n_depts));
+  const int units = std::min(c.n_depts, T * dk) +
+                    (c.d_private ? std::min(c.n_experts, T * c.top_k) : 0) +
+                    (c.d_shared_expert ? 1 : 0);
+  return units <= kMaxChainUnits;
+}
+
 template <class P>
 P *at(void *ws, size_t off) {
   return reinterpret_cast<P *>(static_cast<char *>(ws) + off);
@@ -279,6 +304,11 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.zsbuf = at<void>(ws, L.zsbuf);
   a.zbuf = at<float>(ws, L.zbuf);
   a.partial = at<float>(ws, L.partial);
+  if (plan == PLAN_SLICE && use_chain(c, T)) {
+    a.chain = 1;
+    a.cunits = at<ChainUnit>(ws, L.cunits);
+    a.wdense = at<float>(ws, L.wdense);
+  }
   DEAMOE_TRY(launch_route(a, s));
   DEAMOE_TRY(ev.mark());
   return DEAMOE_OK;
@@ -369,6 +399,18 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
                    se * tiles_bound(1, c.d_shared_expert);
     DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, ta * groups, kGridCap, s));
     DEAMOE_TRY(ev.mark());
+    if (use_chain(c, T)) {   // down projections and combine in one kernel
+      ChainArgs ch;
+      ch.units = at<ChainUnit>(ws, L.cunits);
+      ch.counts = pc->stage[1];
+      ch.y = y;
+      ch.T = T;
+      ch.h = c.hidden;
+      ch.act_f32 = c.act_dtype == DEAMOE_F32;
+      DEAMOE_TRY(launch_chain(ch, wt, s));
+      DEAMOE_TRY(ev.mark());
+      return DEAMOE_OK;
+    }
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
     DEAMOE_TRY(launch_down(stage(1), wt, T, down_ks_of(c, T), units, c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
@@ -492,6 +534,15 @@ int deamoe_layer_forward_traced(const deamoe_config *cfg, int32_t T, const void 
                                 int32_t n_events) {
   return layer_impl(cfg, T, x, w, logits_in, router_bias, routing_out, y, ws, ws_bytes, stream,
                     events, n_events);
+}
+
+int deamoe_trace_points(const deamoe_config *cfg, int32_t T, int32_t *n_events) {
+  const int rc = validate_config(cfg);
+  if (rc) return rc;
+  if (!n_events || T < 1 || T > cfg->max_tokens) return DEAMOE_ERR_INVALID;
+  if (cfg->form == DEAMOE_FORM_SLICE) *n_events = use_chain(*cfg, T) ? 5 : 6;
+  else *n_events = 9;
+  return DEAMOE_OK;
 }
 
 int deamoe_baseline_forward(const deamoe_config *cfg, int32_t T, const void *x,

@@ -1,0 +1,212 @@
+// Down projections of the SLICE form fused with the weighted combine of
+// Eq. 3, for batches of at most 16 tokens.
+//
+// For every active unit u (department, expert, shared expert) the gate/up
+// stage has stored a_{t,u} = SiLU(G_u x_t) * (U_u x_t) for the unit's tokens,
+// one row per member token in ascending token order.  The layer output is
+//
+//   y_t = sum_u p_{t,u} W_u a_{t,u}
+//
+// (P_{t,j} for a department, Sec. 3.2), one product over the concatenated K
+// steps of all units in which token t's column carries the weight p_{t,u}
+// and zero for units it does not use.  A workgroup owns 32 rows of y (two
+// 16-row halves sharing the token operand) and splits the concatenated K
+// steps into KSC contiguous ranges, one per wave, so that every wave streams
+// one long run of weight rows; each K step's product is added to the
+// accumulator with the lane's token weight (times the fp8 block scale), and
+// the partial tiles are summed through LDS in wave order and rounded once.
+// No fp32 partial rows and no combine launch.
+#include "gemm_tile.h"
+#include "launch.h"
+
+namespace deamoe {
+
+// One K step of both halves: the step's products start from zero and are
+// added with the per-lane factor f (the token's weight, times the fp8 scale).
+template <int WT>
+__device__ inline void chain_mma(const u32x4 (&a)[2][4], const u32x4 (&b)[4], float f,
+                                 f32x4 (&acc)[2]) {
+#pragma unroll
+  for (int n = 0; n < 2; ++n) {
+    f32x4 t = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (WT == WT_F32) {
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          t = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[n][m][e]),
+                                                   __uint_as_float(b[m][e]), t, 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const bf16x8 w = WT == WT_FP8 ? fp8x8_to_bf16(a[n][m][0], a[n][m][1]) : as_bf16x8(a[n][m]);
+        t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, as_bf16x8(b[m]), t, 0, 0, 0);
+      }
+    }
+    acc[n] += f * t;
+  }
+}
+
+// A 64-bit pointer every lane holds alike, moved to scalar registers.
+template <class P>
+__device__ inline P *uniform_ptr(P *p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<P *>(((uint64_t)hi << 32) | lo);
+}
+
+template <int WT, int KSC, int PF>
+__global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
+  using Tr = WTraits<WT>;
+  using LD = WLoad<WT>;
+  constexpr int NW = 2;            // the two 16-row halves of the tile
+  constexpr int TR = 2 * kTile;    // rows of y per workgroup
+  constexpr int NB = PF + 1;       // load groups per wave: PF in flight, one multiplied
+  constexpr int ASEG = Tr::K_STEP * Tr::A_BYTES;
+  constexpr int STAGE = NW * LD::REGION;
+  constexpr int RED = NW * kWave * 16;
+  constexpr int WB = STAGE > RED ? STAGE : RED;
+  __shared__ __attribute__((aligned(16))) char s_buf[KSC][WB];
+  __shared__ ChainUnit s_u[kMaxChainUnits];
+  const int n_units = uniform(a.counts[0]), S = uniform(a.counts[1]);
+  {
+    const uint32_t *src = reinterpret_cast<const uint32_t *>(a.units);
+    uint32_t *dst = reinterpret_cast<uint32_t *>(s_u);
+    const int nd = n_units * (int)(sizeof(ChainUnit) / 4);
+    for (int i = threadIdx.x; i < nd; i += blockDim.x) dst[i] = src[i];
+  }
+  __syncthreads();
+  const int wave = uniform(threadIdx.x / kWave), lane = lane_id();
+  const int g = lane >> 4, j = lane & 15;
+  const int T = a.T, R = a.h, rt = blockIdx.x;
+  const int lrow = lane / LD::LPR, lchunk = lane % LD::LPR;
+  const int rmax = R - 1 - kTile;   // last row the first half may read
+  const int s_lo = uniform((int)((int64_t)S * wave / KSC));
+  const int total = uniform((int)((int64_t)S * (wave + 1) / KSC)) - s_lo;
+  char *lds = s_buf[wave];
+  f32x4 acc[NW];
+  acc[0] = acc[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (total > 0) {
+    // the unit holding step s_lo: the last one whose first step is <= s_lo
+    int lo = 0, hi = n_units - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (uniform(s_u[mid].step0) <= s_lo) lo = mid; else hi = mid - 1;
+    }
+    int cu = uniform(lo);
+    // issue cursor: unit cu, its K step ck of nk; the unit's per-lane state
+    int ck = s_lo - uniform(s_u[cu].step0), nk = 0, ldw = 0;
+    const char *w0 = nullptr, *bp = nullptr;
+    const float *sp = nullptr, *pp = nullptr;
+    uint64_t mm = 0;   // lanes whose token is a member of the unit
+    const uint32_t tmask = T >= 32 ? 0xffffffffu : (1u << T) - 1u;
+    auto load_unit = [&](int u) {
+      ldw = uniform(s_u[u].K);
+      nk = ldw / Tr::K_STEP;
+      w0 = static_cast<const char *>(uniform_ptr(s_u[u].w)) + lchunk * 16;
+      const uint32_t m16 = (uint32_t)uniform((int)s_u[u].mask) & tmask & 0xffffu;
+      mm = (uint64_t)m16 * 0x0001000100010001ull;
+      // a member's row is its rank among the members; other lanes read the
+      // first member's row (their weight is zero), so each load touches only
+      // the unit's rows
+      const int rank = (m16 >> j) & 1 ? __popc(m16 & ((1u << j) - 1u)) : 0;
+      bp = static_cast<const char *>(uniform_ptr(s_u[u].in)) + (size_t)rank * ldw * Tr::A_BYTES;
+      pp = uniform_ptr(s_u[u].pw) + j;
+      if constexpr (WT == WT_FP8)   // the tile's 32 rows lie in one scale row
+        sp = uniform_ptr(s_u[u].s) + (size_t)((rt * TR) / 128) * (ldw / 128);
+    };
+    load_unit(cu);
+    // loads past the wave's range read cache-resident data of the first unit
+    const char *dummy = bp + (lane & 15) * 16;
+    const char *dummy_b = bp;
+    const float *dummy_s = sp, *dummy_p = pp;
+    u32x4 G[NB][NW][LD::NQ];
+    u32x4 B[NB][4];
+    uint64_t MM[NB];
+    float SC[NB], P[NB];
+    auto issue = [&](u32x4(&Gb)[NW][LD::NQ], u32x4(&Bb)[4], uint64_t &mms, float &sc, float &pw,
+                     int v) {
+      const bool ok = v < total;
+      if (ok && ck == nk) {   // the previous step ended a unit
+        ++cu;
+        ck = 0;
+        load_unit(cu);
+      }
+#pragma unroll
+      for (int q = 0; q < LD::NQ; ++q) {
+        const int row = min(rt * TR + q * LD::RPI + lrow, rmax);
+        const size_t woff = (size_t)row * ldw * Tr::W_BYTES + (size_t)ck * LD::WSEG;
+        const size_t half = (size_t)kTile * ldw * Tr::W_BYTES;
+        Gb[0][q] = __builtin_nontemporal_load(gptr(ok ? w0 + woff : dummy));
+        Gb[1][q] = __builtin_nontemporal_load(gptr(ok ? w0 + woff + half : dummy));
+      }
+      const char *b = ok ? bp + (size_t)ck * ASEG : dummy_b;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) Bb[q] = *gptr(b + b_chunk_offset(g, q));
+      pw = *gfptr(ok ? pp : dummy_p);
+      if constexpr (WT == WT_FP8) sc = *gfptr(ok ? sp + ck : dummy_s);
+      mms = mm;
+      if (ok) ++ck;
+    };
+#pragma unroll
+    for (int p = 0; p < PF; ++p) issue(G[p], B[p], MM[p], SC[p], P[p], p);
+    for (int v = 0;;) {
+#pragma unroll
+      for (int q = 0; q < NB; ++q) {
+        const int qn = (q + NB - 1) % NB;   // the buffer consumed one step ago
+        issue(G[qn], B[qn], MM[qn], SC[qn], P[qn], v + PF);
+        __builtin_amdgcn_sched_barrier(0);
+        u32x4 w[NW][4];
+        stage_weights<WT, NW>(lds, G[q], w);
+        // tokens outside the unit have weight zero (their operand is a
+        // member's row, so the product is finite)
+        const float f0 = (MM[q] >> lane) & 1 ? P[q] : 0.f;
+        chain_mma<WT>(w, B[q], WT == WT_FP8 ? f0 * SC[q] : f0, acc);
+        __builtin_amdgcn_sched_barrier(0);
+        if (++v >= total) goto streamed;
+      }
+    }
+  }
+streamed:
+  // partial tiles summed in wave order; wave 0 rounds and stores
+  __syncthreads();   // every wave is done with its staging region
+  f32x4 *red = reinterpret_cast<f32x4 *>(s_buf[wave]);
+  if (wave > 0) {
+    red[lane] = acc[0];
+    red[kWave + lane] = acc[1];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    for (int q = 1; q < KSC; ++q) {
+      const f32x4 *r = reinterpret_cast<const f32x4 *>(s_buf[q]);
+      acc[0] += r[lane];
+      acc[1] += r[kWave + lane];
+    }
+    const int row0 = rt * TR + 4 * g;
+    if (j < T) {
+      const size_t off = (size_t)j * R + row0;
+      if (row0 < R) store4(a.y, a.act_f32, off, acc[0], row0 + 3 < R, R - row0);
+      const int row1 = row0 + kTile;
+      if (row1 < R) store4(a.y, a.act_f32, off + kTile, acc[1], row1 + 3 < R, R - row1);
+    }
+  }
+}
+
+template <int WT>
+static hipError_t launch_chain_wt(const ChainArgs &a, hipStream_t s) {
+  const dim3 grid((a.h + 2 * kTile - 1) / (2 * kTile));
+  constexpr int KSC = DEAMOE_CHAIN_WAVES, PF = DEAMOE_CHAIN_PF;
+  hipLaunchKernelGGL((chain_down_kernel<WT, KSC, PF>), grid, dim3(KSC * kWave), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_chain(const ChainArgs &a, int wtype, hipStream_t s) {
+  switch (wtype) {
+    case WT_F32: return launch_chain_wt<WT_F32>(a, s);
+    case WT_BF16: return launch_chain_wt<WT_BF16>(a, s);
+    default: return launch_chain_wt<WT_FP8>(a, s);
+  }
+}
+
+}  // namespace deamoe

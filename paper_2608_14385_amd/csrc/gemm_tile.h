@@ -145,6 +145,38 @@ __device__ inline void step_mma(const u32x4 (&a)[NW][4], const u32x4 (&B)[NTT][S
   }
 }
 
+// Rows of one staged K step (as loaded: instruction q covers rows
+// q * RPI + lane / LPR, 16 bytes each) written to the wave's LDS region and
+// read back in the matrix-core operand layout.
+template <int WT, int NW>
+__device__ inline void stage_weights(char *lds, const u32x4 (&Gb)[NW][WLoad<WT>::NQ],
+                                     u32x4 (&a)[NW][4]) {
+  using LD = WLoad<WT>;
+  const int lane = lane_id();
+  const int g = lane >> 4, j = lane & 15;
+  const int lrow = lane / LD::LPR, lchunk = lane % LD::LPR;
+#pragma unroll
+  for (int n = 0; n < NW; ++n)
+#pragma unroll
+    for (int q = 0; q < LD::NQ; ++q)
+      *reinterpret_cast<u32x4 *>(lds + n * LD::REGION + (q * LD::RPI + lrow) * LD::RS +
+                                 lchunk * 16) = Gb[n][q];
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int n = 0; n < NW; ++n)
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      if constexpr (WT == WT_FP8) {
+        const u32x2 v = *reinterpret_cast<const u32x2 *>(lds + n * LD::REGION + j * LD::RS +
+                                                           m * 32 + g * 8);
+        a[n][m] = u32x4{v[0], v[1], 0u, 0u};
+      } else {
+        a[n][m] = *reinterpret_cast<const u32x4 *>(lds + n * LD::REGION + j * LD::RS +
+                                                      b_chunk_offset(g, m));
+      }
+    }
+}
+
 // Stream one work item: row tiles rt0 .. rt0 + nsub - 1 of unit U, each over
 // the K steps kp, kp + ks, ... (nsub > 1 only when ks == 1).  PAIR: a tile is
 // 32 rows of one matrix, streamed as two 16-row halves (w0 and w0 + 16 rows)
@@ -230,28 +262,8 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
     if constexpr (WT == WT_FP8)   // a row pair lies in one scale row
       sc = uniform((((rt0 + sub) * TR) / 128 - srow0) * sblocks + kstep);
   };
-  // rows of the staged step in the matrix-core operand layout
   auto stage = [&](const u32x4(&Gb)[NW][LD::NQ], u32x4(&a)[NW][4]) {
-#pragma unroll
-    for (int n = 0; n < NW; ++n)
-#pragma unroll
-      for (int q = 0; q < LD::NQ; ++q)
-        *reinterpret_cast<u32x4 *>(lds + n * LD::REGION + (q * LD::RPI + lrow) * LD::RS +
-                                       lchunk * 16) = Gb[n][q];
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int n = 0; n < NW; ++n)
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        if constexpr (WT == WT_FP8) {
-          const u32x2 v = *reinterpret_cast<const u32x2 *>(lds + n * LD::REGION + j * LD::RS +
-                                                             m * 32 + g * 8);
-          a[n][m] = u32x4{v[0], v[1], 0u, 0u};
-        } else {
-          a[n][m] = *reinterpret_cast<const u32x4 *>(lds + n * LD::REGION + j * LD::RS +
-                                                        b_chunk_offset(g, m));
-        }
-      }
+    stage_weights<WT, NW>(lds, Gb, a);
   };
 #pragma unroll
   for (int p = 0; p < PF; ++p) issue(G[p], B[p], SC[p], p);

@@ -44,6 +44,15 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define DEAMOE_FDOWN_KS2_T 16
 #endif
 
+// Fused SLICE down stage: waves per workgroup (each streams one contiguous
+// range of the concatenated K steps) and load groups in flight per wave.
+#ifndef DEAMOE_CHAIN_WAVES
+#define DEAMOE_CHAIN_WAVES 8
+#endif
+#ifndef DEAMOE_CHAIN_PF
+#define DEAMOE_CHAIN_PF 1
+#endif
+
 constexpr int kWave = 64;
 constexpr int kTile = 16;   // MFMA tile edge: 16 weight rows x 16 tokens
 
@@ -71,6 +80,22 @@ struct GemmUnit {
   int32_t epi;              // Epilogue
   int32_t out_f32;          // 1: outputs are fp32, 0: act dtype
   int32_t tpg;              // row tiles per work item (1 unless the K split is 1)
+};
+
+// One unit of the fused down projection and combine of the SLICE form (at
+// most 16 tokens): the [R, K] down matrix w (fp8: block scales s) applied to
+// the unit's gate/up outputs `in` ([members, K], one row per member token in
+// ascending token order), each token's product weighted by pw[t].  The K
+// steps of all units form one concatenation.
+struct ChainUnit {
+  const void *w;
+  const float *s;
+  const void *in;
+  const float *pw;          // routing weight of token t at pw[t] (members only)
+  int32_t K;
+  uint32_t mask;            // member tokens, bit t
+  int32_t step0;            // first K step of the unit in the concatenation
+  int32_t pad_;
 };
 
 struct GemmStage {

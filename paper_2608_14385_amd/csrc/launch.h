@@ -61,6 +61,11 @@ struct RouteArgs {
   void *gbuf, *ubuf, *ybuf, *zsbuf;           // FACTORED intermediates (act dtype)
   float *zbuf;                                // FACTORED sigma(A_d^T Y), fp32
   float *partial;                             // [pairs, h] fp32
+  // SLICE at most 16 tokens: down projections fused with the combine
+  int32_t chain;
+  ChainUnit *cunits;                          // units of the fused down stage
+  float *wdense;                              // [m + n + 1][16] routing weight per unit and
+                                              // token (last row: the shared expert's 1)
 };
 
 struct CombineArgs {
@@ -69,6 +74,16 @@ struct CombineArgs {
   const float *slot_w;
   void *y;
   int32_t T, h, max_slots, act_f32;
+};
+
+// Fused down projection and combine (SLICE form, T <= 16): one workgroup per
+// 32 rows of y.
+constexpr int kMaxChainUnits = 512;
+struct ChainArgs {
+  const ChainUnit *units;
+  const int32_t *counts;    // [0] = number of units, [1] = K steps of the concatenation
+  void *y;                  // [T, h] act dtype
+  int32_t T, h, act_f32;
 };
 
 struct ZsumArgs {
@@ -104,6 +119,7 @@ enum GemmMode : int {
 hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int mode, int ntt,
                                int ks, int max_tiles, int grid_cap, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
+hipError_t launch_chain(const ChainArgs &a, int wtype, hipStream_t s);
 hipError_t launch_zsum(const ZsumArgs &a, int max_dept_pairs, hipStream_t s);
 
 }  // namespace deamoe

@@ -280,6 +280,12 @@ __device__ inline void put_unit(gmem<GemmUnit> *U, const void *w0, const void *w
   U->out_f32 = out_f32; U->tpg = tpg;
 }
 
+__device__ inline void put_chain(gmem<ChainUnit> *U, const void *w, const float *s, const void *in,
+                                 const float *pw, int K, uint32_t mask, int step0) {
+  U->w = w; U->s = s; U->in = in; U->pw = pw; U->K = K; U->mask = mask; U->step0 = step0;
+  U->pad_ = 0;
+}
+
 // Row tiles per work item of a stage whose K is not split across waves: short
 // contractions take several tiles so that a work item streams enough bytes.
 __device__ inline int tiles_per_item(int K, int rows, int ks) {
@@ -586,6 +592,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     a.r.topk_ids[t * k + lane] = my_id;
     if (lds.ids) lds.ids[t * k + lane] = my_id;
     a.r.topk_w[t * k + lane] = p;
+    if (a.wdense) a.wdense[(size_t)(a.m + my_id) * kTile + t] = p;
     atomicOr(&s_db[d >> 5], 1u << (d & 31));
   }
   wave_lds_sync();
@@ -610,6 +617,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     a.r.tok_depts[t * k + dpos] = d;
     if (lds.dep) lds.dep[t * k + dpos] = d;
     a.r.tok_dept_w[t * k + dpos] = P;
+    if (a.wdense) a.wdense[(size_t)d * kTile + t] = P;
     if (a.plan) a.slot_w[(size_t)t * S + dpos] = slice ? P : 1.0f;
   }
   if (lane >= nd && lane < k) {
@@ -828,6 +836,10 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
     const int gd = tiles_per_item(a.d_s, dr, dk), gp = a.d_p ? tiles_per_item(a.d_p, dr, dk) : 1;
     const int gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
     const int bse = items_of(a.h, gse, dr);
+    // fused down stage (T <= 16): the units' K steps are concatenated in
+    // table order (departments, experts, the shared expert)
+    const int kstep = a.w_bytes == 4 ? 64 : 128;
+    const int sd = a.d_s / kstep, sp = a.d_p / kstep;
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_scan[j] >> 16, off = doff(j);
       const int32_t *idx = a.r.dept_tokens + off;
@@ -835,10 +847,15 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
       put_unit(glob(a.units[0]) + u, wptr(W.dept_gate, j, a.d_s, a.h), wptr(W.dept_up, j, a.d_s, a.h),
                sptr(W.scale[0], j, a.d_s, a.h), sptr(W.scale[1], j, a.d_s, a.h), x, x, idx, ao,
                nullptr, a.d_s, a.h, a.h, a.d_s, my_dc, dbeg_a(j, u), EPI_SWIGLU, a.act_f32);
-      put_unit(glob(a.units[1]) + u, wptr(W.dept_down, j, a.h, a.d_s), nullptr,
-               sptr(W.scale[2], j, a.h, a.d_s), nullptr, ao, ao, nullptr,
-               a.partial + (size_t)off * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, my_dc,
-               dbeg_b(j, u), EPI_STORE, 1, gd);
+      if (a.chain)
+        put_chain(glob(a.cunits) + u, wptr(W.dept_down, j, a.h, a.d_s),
+                  sptr(W.scale[2], j, a.h, a.d_s), ao, a.wdense + (size_t)j * kTile, a.d_s,
+                  s_dtok[j * kTW], u * sd);
+      else
+        put_unit(glob(a.units[1]) + u, wptr(W.dept_down, j, a.h, a.d_s), nullptr,
+                 sptr(W.scale[2], j, a.h, a.d_s), nullptr, ao, ao, nullptr,
+                 a.partial + (size_t)off * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, my_dc,
+                 dbeg_b(j, u), EPI_STORE, 1, gd);
     }
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
@@ -851,20 +868,36 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                sptr(W.scale[3], e, a.d_p, a.h), sptr(W.scale[4], e, a.d_p, a.h), x, x, idx, ao,
                nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q], ebeg_a(e, ui), EPI_SWIGLU,
                a.act_f32);
-      put_unit(glob(a.units[1]) + u, wptr(W.priv_down, e, a.h, a.d_p), nullptr,
-               sptr(W.scale[5], e, a.h, a.d_p), nullptr, ao, ao, nullptr,
-               a.partial + (size_t)(ndp + off) * a.h, nullptr, a.h, a.d_p, a.d_p, a.h, my_ec[q],
-               ebeg_b(e, ui), EPI_STORE, 1, gp);
+      if (a.chain)
+        put_chain(glob(a.cunits) + u, wptr(W.priv_down, e, a.h, a.d_p),
+                  sptr(W.scale[5], e, a.h, a.d_p), ao, a.wdense + (size_t)(m + e) * kTile, a.d_p,
+                  s_etok[e * kTW], ud * sd + ui * sp);
+      else
+        put_unit(glob(a.units[1]) + u, wptr(W.priv_down, e, a.h, a.d_p), nullptr,
+                 sptr(W.scale[5], e, a.h, a.d_p), nullptr, ao, ao, nullptr,
+                 a.partial + (size_t)(ndp + off) * a.h, nullptr, a.h, a.d_p, a.d_p, a.h,
+                 my_ec[q], ebeg_b(e, ui), EPI_STORE, 1, gp);
     }
+    // weight 1 of the shared expert: the row after the experts'
+    if (a.chain && tid < kTile) a.wdense[(size_t)(m + n) * kTile + tid] = 1.0f;
     if (tid == 0) {
       int units = ud + ue, items_a = tot_a, items_b = tot_b;
+      int steps = ud * sd + ue * sp;
       if (has_se) {
         put_unit(glob(a.units[0]) + units, W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
                  a.h, a.d_se, T, items_a, EPI_SWIGLU, a.act_f32);
-        put_unit(glob(a.units[1]) + units, W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se), nullptr,
-                 a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)(ndp + nep_priv) * a.h,
-                 nullptr, a.h, a.d_se, a.d_se, a.h, T, items_b, EPI_STORE, 1, gse);
+        if (a.chain) {
+          put_chain(glob(a.cunits) + units, W.se_down, sptr(W.scale[8], 0, a.h, a.d_se), a.abuf_se,
+                    a.wdense + (size_t)(m + n) * kTile, a.d_se,
+                    T >= 32 ? 0xffffffffu : (1u << T) - 1u, steps);
+          steps += a.d_se / kstep;
+        } else {
+          put_unit(glob(a.units[1]) + units, W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
+                   nullptr, a.abuf_se, a.abuf_se, nullptr,
+                   a.partial + (size_t)(ndp + nep_priv) * a.h, nullptr, a.h, a.d_se, a.d_se, a.h,
+                   T, items_b, EPI_STORE, 1, gse);
+        }
         items_a += (a.d_se + kTile - 1) / kTile * groups(T);
         items_b += bse * groups(T);
         ++units;
@@ -872,7 +905,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
       counts->stage[0][0] = units;
       counts->stage[0][1] = items_a;
       counts->stage[1][0] = units;
-      counts->stage[1][1] = items_b;
+      counts->stage[1][1] = a.chain ? steps : items_b;
     }
   } else {  // PLAN_FACTORED
     const int d = a.d_s;

@@ -25,7 +25,7 @@ MAX_TOKENS = 128
 
 EXPORTS = ("deamoe_status_string", "deamoe_workspace_bytes", "deamoe_route",
            "deamoe_layer_forward", "deamoe_layer_forward_traced", "deamoe_baseline_forward",
-           "deamoe_loaded_bytes")
+           "deamoe_loaded_bytes", "deamoe_trace_points")
 
 
 class DeamoeError(RuntimeError):
@@ -78,6 +78,7 @@ def lib():
         L.deamoe_layer_forward.argtypes = layer_args
         L.deamoe_baseline_forward.argtypes = layer_args
         L.deamoe_layer_forward_traced.argtypes = layer_args + [C.POINTER(C.c_void_p), i32]
+        L.deamoe_trace_points.argtypes = [cfgp, i32, C.POINTER(C.c_int32)]
         L.deamoe_loaded_bytes.argtypes = [cfgp, i32, vp, vp, C.POINTER(C.c_int64),
                                           C.POINTER(C.c_int64)]
         for f in EXPORTS:
@@ -218,6 +219,12 @@ def deamoe_loaded_bytes(c: deamoe_config, T: int, dept_count, exp_count) -> tupl
     _check(lib().deamoe_loaded_bytes(C.byref(c), T, dc.ctypes.data, ec.ctypes.data, C.byref(wb),
                                      C.byref(tb)), "deamoe_loaded_bytes")
     return int(wb.value), int(tb.value)
+
+
+def deamoe_trace_points(c: deamoe_config, T: int) -> int:
+    n = C.c_int32(0)
+    _check(lib().deamoe_trace_points(C.byref(c), T, C.byref(n)), "deamoe_trace_points")
+    return int(n.value)
 
 
 class Layer:

@@ -73,6 +73,35 @@ def test_small_variants(variant):
     check_case(case)
 
 
+@pytest.mark.parametrize("variant", ["f32_t13_se", "f32_t16_no_private", "f32_t7_group_limited",
+                                     "bf16_t16_sigmoid", "fp8_t11_se", "f32_baseline_t9"])
+def test_fused_down_combine(variant):
+    """Down projections and combine in one kernel (SLICE, at most 16 tokens,
+    hidden 4096 = 128 tiles of 32 rows): ragged batches, a shared expert, no
+    private part, a group-limited gate, bf16 and fp8 weights (32 scale rows,
+    4 scale blocks per department contraction) and the vanilla layer; every
+    output checked."""
+    base = small(hidden=4096)
+    baseline = False
+    if variant == "f32_t13_se":
+        case = Case(base.replace(d_shared_expert=192), 13, seed=41)
+    elif variant == "f32_t16_no_private":
+        case = Case(base.replace(d_private=0), 16, seed=42)
+    elif variant == "f32_t7_group_limited":
+        case = Case(base.replace(n_experts=64, n_depts=8, top_k=6, top_k_dept=3), 7, seed=43)
+    elif variant == "bf16_t16_sigmoid":
+        case = Case(base.replace(w_dtype="bf16", act_dtype="bf16", score="sigmoid", d_private=128),
+                    16, seed=44)
+    elif variant == "fp8_t11_se":
+        case = Case(base.replace(w_dtype="fp8", act_dtype="bf16", d_private=256,
+                                 d_shared_expert=256), 11, seed=45)
+    else:
+        cfg = base.replace(name="small_baseline", n_depts=16, d_shared=576, d_private=0)
+        case, baseline = Case(cfg, 9, seed=46), True
+    assert D.deamoe_trace_points(D.make_config(case.cfg, case.T), case.T) == 5   # fused path
+    check_case(case, baseline=baseline)
+
+
 @pytest.mark.parametrize("T", [1, 4, 19])
 def test_tiny_factored(T):
     check_case(Case(P["tiny_factored"].layer, T, seed=10 + T))
