@@ -179,9 +179,10 @@ int deamoe_layer_forward(const deamoe_config *cfg, int32_t T, const void *x,
 /* The same with caller-created hipEvent_t handles recorded on `stream` at the
  * stage boundaries, for timing: events[0] before the router, then one after
  * each launched kernel in order (SLICE: router GEMV, route, gate/up, down,
- * combine, where batches of at most 16 tokens run down and combine as one
- * kernel; FACTORED: router GEMV, route, department gate/up, private gate/up,
- * private down, Z collect, department down, combine).  n_events may be
+ * combine; FACTORED: router GEMV, route, department gate/up, private gate/up,
+ * private down, Z collect, department down, combine).  Batches of at most
+ * 16 tokens may run the last down stage and the combine as one kernel
+ * (deamoe_trace_points gives the count).  n_events may be
  * smaller than that count; NULL / 0 records nothing.  With injected logits
  * the router GEMV is not launched and has no boundary. */
 int deamoe_layer_forward_traced(const deamoe_config *cfg, int32_t T, const void *x,

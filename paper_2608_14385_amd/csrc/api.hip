@@ -94,12 +94,7 @@ Layout make_layout(const deamoe_config &c) {
     L.abuf_exp = take(epairs * dp * ab);
     L.gbuf = L.ubuf = L.ybuf = L.zbuf = L.zsbuf = 0;
     L.partial = take((dpairs + (dp ? epairs : 0) + (dse ? T : 0)) * h * 4);
-    // fused down stage, batches of at most 16 tokens: routing weights per
-    // unit and token, the unit table
-    L.wdense = take((m + n + 1) * kTile * 4);
-    L.cunits = take((size_t)kMaxChainUnits * sizeof(ChainUnit));
   } else {
-    L.wdense = L.cunits = 0;
     L.abuf_dept = L.abuf_exp = 0;
     L.gbuf = take(dpairs * ds * ab);
     L.ubuf = take(dpairs * ds * ab);
@@ -108,6 +103,10 @@ Layout make_layout(const deamoe_config &c) {
     L.zsbuf = take(dpairs * ds * ab);
     L.partial = take((dpairs + (dse ? T : 0)) * h * 4);
   }
+  // fused down stage, batches of at most 16 tokens: routing weights per unit
+  // and token (and a row of ones), the unit table
+  L.wdense = take((m + n + 1) * kTile * 4);
+  L.cunits = take((size_t)kMaxChainUnits * sizeof(ChainUnit));
   L.total = off;
   return L;
 }
@@ -193,21 +192,29 @@ int down_ks_of(const deamoe_config &c, int T) {
 }
 
 
-// Down projections and combine fused into one kernel (SLICE form): batches of
-// at most 16 tokens whose active units fit the kernel's unit table.  Its grid
-// is one workgroup per 32 rows of y; below kChainMinTiles of them (a hidden
-// size under 4096) it is used up to 4 tokens only, where the separate down
-// stage has too few work items to do better (measured on the 2048-wide layer).
+// Down projections and combine fused into one kernel (the SLICE down stage,
+// the FACTORED department down stage): batches of at most 16 tokens whose
+// active units fit the kernel's unit table.  Its grid is one workgroup per 32
+// rows of y.  SLICE: below kChainMinTiles of them (a hidden size under 4096)
+// it is used up to 4 tokens only, where the separate down stage has too few
+// work items to do better (measured on the 2048-wide layer).  FACTORED: the
+// department down stage is a few long contractions that the split-K stage
+// already streams well; the fused kernel gains only with a grid of at least
+// kChainMinTilesFactored workgroups (measured on the 7168- and 4096-wide
+// Table 1 layers).
 #ifndef DEAMOE_CHAIN
 #define DEAMOE_CHAIN 1
 #endif
-constexpr int kChainMinTiles = 128;
+constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 192;
 bool use_chain(const deamoe_config &c, int T) {
-  if (!DEAMOE_CHAIN || c.form != DEAMOE_FORM_SLICE || T > kTile) return false;
-  if (T > 4 && c.hidden / (2 * kTile) < kChainMinTiles) return false;
+  if (!DEAMOE_CHAIN || T > kTile) return false;
+  const int tiles = c.hidden / (2 * kTile);
+  if (c.form == DEAMOE_FORM_FACTORED && tiles < kChainMinTilesFactored) return false;
+  if (T > 4 && tiles < kChainMinTiles) return false;
   const int dk = std::min(c.top_k_dept > 0 ? c.top_k_dept : c.top_k, std::min(c.top_k, c.n_depts));
+  const bool slice_priv = c.form == DEAMOE_FORM_SLICE && c.d_private > 0;
   const int units = std::min(c.n_depts, T * dk) +
-                    (c.d_private ? std::min(c.n_experts, T * c.top_k) : 0) +
+                    (slice_priv ? std::min(c.n_experts, T * c.top_k) : 0) +
                     (c.d_shared_expert ? 1 : 0);
   return units <= kMaxChainUnits;
 }
@@ -304,7 +311,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.zsbuf = at<void>(ws, L.zsbuf);
   a.zbuf = at<float>(ws, L.zbuf);
   a.partial = at<float>(ws, L.partial);
-  if (plan == PLAN_SLICE && use_chain(c, T)) {
+  if (plan != PLAN_NONE && use_chain(c, T)) {
     a.chain = 1;
     a.cunits = at<ChainUnit>(ws, L.cunits);
     a.wdense = at<float>(ws, L.wdense);
@@ -450,6 +457,18 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     za.rms = c.sigma == DEAMOE_SIGMA_RMSNORM;
     DEAMOE_TRY(launch_zsum(za, T * dk, s));
     DEAMOE_TRY(ev.mark());
+    if (use_chain(c, T)) {   // department down projections and combine in one kernel
+      ChainArgs ch;
+      ch.units = at<ChainUnit>(ws, L.cunits);
+      ch.counts = pc->stage[3];
+      ch.y = y;
+      ch.T = T;
+      ch.h = c.hidden;
+      ch.act_f32 = c.act_dtype == DEAMOE_F32;
+      DEAMOE_TRY(launch_chain(ch, wt, s));
+      DEAMOE_TRY(ev.mark());
+      return DEAMOE_OK;
+    }
     DEAMOE_TRY(launch_down(stage(3), wt, T, down_ks_of(c, T), act_depts + se, c.hidden, kGridCap,
                            s));
     DEAMOE_TRY(ev.mark());
@@ -540,8 +559,7 @@ int deamoe_trace_points(const deamoe_config *cfg, int32_t T, int32_t *n_events) 
   const int rc = validate_config(cfg);
   if (rc) return rc;
   if (!n_events || T < 1 || T > cfg->max_tokens) return DEAMOE_ERR_INVALID;
-  if (cfg->form == DEAMOE_FORM_SLICE) *n_events = use_chain(*cfg, T) ? 5 : 6;
-  else *n_events = 9;
+  *n_events = (cfg->form == DEAMOE_FORM_SLICE ? 6 : 9) - (use_chain(*cfg, T) ? 1 : 0);
   return DEAMOE_OK;
 }
 

@@ -832,13 +832,13 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
   auto ebeg_b = [&](int e, int ui) { return multi ? s_ib[m + e] : ud * ib_d + ui * ib_e; };
   const int dept_a = multi ? s_ia[m] : ud * ia_d;   // items of all departments
   const int dept_b = multi ? s_ib[m] : ud * ib_d;
+  const int kstep = a.w_bytes == 4 ? 64 : 128;   // K step of the weight type
   if (slice) {
     const int gd = tiles_per_item(a.d_s, dr, dk), gp = a.d_p ? tiles_per_item(a.d_p, dr, dk) : 1;
     const int gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
     const int bse = items_of(a.h, gse, dr);
     // fused down stage (T <= 16): the units' K steps are concatenated in
     // table order (departments, experts, the shared expert)
-    const int kstep = a.w_bytes == 4 ? 64 : 128;
     const int sd = a.d_s / kstep, sp = a.d_p / kstep;
     if (tid < m && my_dc > 0) {
       const int j = tid, u = s_scan[j] >> 16, off = doff(j);
@@ -921,9 +921,14 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
       put_unit(glob(a.units[0]) + u, wptr(W.dept_gate, j, d, a.h), wptr(W.dept_up, j, d, a.h),
                sptr(W.scale[0], j, d, a.h), sptr(W.scale[1], j, d, a.h), x, x, idx, go, uo, d,
                a.h, a.h, d, my_dc, dbeg_a(j, u), EPI_SIGMA2, a.act_f32);
-      put_unit(glob(a.units[3]) + u, wptr(W.dept_down, j, a.h, d), nullptr, sptr(W.scale[2], j, a.h, d),
-               nullptr, zs, zs, nullptr, a.partial + (size_t)off * a.h, nullptr, a.h, d, d,
-               a.h, my_dc, dbeg_b(j, u), EPI_STORE, 1, gd);
+      if (a.chain)   // Z already carries the routing weights: unit weight 1
+        put_chain(glob(a.cunits) + u, wptr(W.dept_down, j, a.h, d), sptr(W.scale[2], j, a.h, d), zs,
+                  a.wdense + (size_t)(m + n) * kTile, d, s_dtok[j * kTW], u * (d / kstep));
+      else
+        put_unit(glob(a.units[3]) + u, wptr(W.dept_down, j, a.h, d), nullptr,
+                 sptr(W.scale[2], j, a.h, d), nullptr, zs, zs, nullptr,
+                 a.partial + (size_t)off * a.h, nullptr, a.h, d, d, a.h, my_dc, dbeg_b(j, u),
+                 EPI_STORE, 1, gd);
     }
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
@@ -939,20 +944,30 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                nullptr, yo, yo, nullptr, a.zbuf + (size_t)off * d, nullptr, d, d, d, d,
                my_ec[q], ebeg_b(e, u) - dept_b, EPI_SIGMA, 1, g2);
     }
+    if (a.chain && tid < kTile) a.wdense[(size_t)(m + n) * kTile + tid] = 1.0f;
     if (tid == 0) {
       int units0 = ud, items0 = dept_a, units3 = ud, items3 = dept_b;
+      int steps = ud * (d / kstep);
       if (has_se) {
         put_unit(glob(a.units[0]) + units0, W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
                  sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
                  a.h, a.d_se, T, items0, EPI_SWIGLU, a.act_f32);
-        put_unit(glob(a.units[3]) + units3, W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
-                 nullptr, a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)ndp * a.h, nullptr,
-                 a.h, a.d_se, a.d_se, a.h, T, items3, EPI_STORE, 1, gse);
+        if (a.chain) {
+          put_chain(glob(a.cunits) + units3, W.se_down, sptr(W.scale[8], 0, a.h, a.d_se), a.abuf_se,
+                    a.wdense + (size_t)(m + n) * kTile, a.d_se,
+                    T >= 32 ? 0xffffffffu : (1u << T) - 1u, steps);
+          steps += a.d_se / kstep;
+        } else {
+          put_unit(glob(a.units[3]) + units3, W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
+                   nullptr, a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)ndp * a.h,
+                   nullptr, a.h, a.d_se, a.d_se, a.h, T, items3, EPI_STORE, 1, gse);
+        }
         ++units0;
         items0 += (a.d_se + kTile - 1) / kTile * groups(T);
         ++units3;
         items3 += bse * groups(T);
       }
+      if (a.chain) items3 = steps;
       counts->stage[0][0] = units0;
       counts->stage[0][1] = items0;
       counts->stage[1][0] = ue;

@@ -74,13 +74,15 @@ def test_small_variants(variant):
 
 
 @pytest.mark.parametrize("variant", ["f32_t13_se", "f32_t16_no_private", "f32_t7_group_limited",
-                                     "bf16_t16_sigmoid", "fp8_t11_se", "f32_baseline_t9"])
+                                     "bf16_t16_sigmoid", "fp8_t11_se", "f32_baseline_t9",
+                                     "factored_t13_se_rmsnorm", "factored_fp8_t16"])
 def test_fused_down_combine(variant):
-    """Down projections and combine in one kernel (SLICE, at most 16 tokens,
-    hidden 4096 = 128 tiles of 32 rows): ragged batches, a shared expert, no
-    private part, a group-limited gate, bf16 and fp8 weights (32 scale rows,
-    4 scale blocks per department contraction) and the vanilla layer; every
-    output checked."""
+    """The last down stage and the combine in one kernel (at most 16 tokens,
+    hidden 4096 = 128 tiles of 32 rows; FACTORED 6144 = 192 tiles): ragged
+    batches, a shared expert, no private part, a group-limited gate, bf16 and
+    fp8 weights (32 scale rows, 4 scale blocks per department contraction),
+    the vanilla layer, and the FACTORED W_d^T stage (RMSNorm sigma, fp8);
+    every output checked."""
     base = small(hidden=4096)
     baseline = False
     if variant == "f32_t13_se":
@@ -95,10 +97,18 @@ def test_fused_down_combine(variant):
     elif variant == "fp8_t11_se":
         case = Case(base.replace(w_dtype="fp8", act_dtype="bf16", d_private=256,
                                  d_shared_expert=256), 11, seed=45)
-    else:
+    elif variant == "f32_baseline_t9":
         cfg = base.replace(name="small_baseline", n_depts=16, d_shared=576, d_private=0)
         case, baseline = Case(cfg, 9, seed=46), True
-    assert D.deamoe_trace_points(D.make_config(case.cfg, case.T), case.T) == 5   # fused path
+    elif variant == "factored_t13_se_rmsnorm":   # W_d^T Z with the weights already in Z
+        case = Case(base.replace(hidden=6144, form="factored", d_shared=256, d_private=0,
+                                 d_shared_expert=128, sigma="rmsnorm"), 13, seed=47)
+    else:
+        case = Case(base.replace(hidden=6144, form="factored", d_shared=256, d_private=0,
+                                 w_dtype="fp8", act_dtype="bf16", score="sigmoid", top_k=4), 16,
+                    seed=48)
+    fused = 5 if case.cfg.form == "slice" else 8
+    assert D.deamoe_trace_points(D.make_config(case.cfg, case.T), case.T) == fused
     check_case(case, baseline=baseline)
 
 
