@@ -180,8 +180,8 @@ int deamoe_layer_forward(const deamoe_config *cfg, int32_t T, const void *x,
  * stage boundaries, for timing: events[0] before the router, then one after
  * each launched kernel in order (SLICE: router GEMV, route, gate/up, down,
  * combine; FACTORED: router GEMV, route, department gate/up, private gate/up,
- * private down, Z collect, department down, combine).  Batches of at most
- * 16 tokens may run the last down stage and the combine as one kernel
+ * private down, Z collect, department down, combine).  Small batches may
+ * run the last down stage and the combine as one kernel
  * (deamoe_trace_points gives the count).  n_events may be
  * smaller than that count; NULL / 0 records nothing.  With injected logits
  * the router GEMV is not launched and has no boundary. */

@@ -103,9 +103,9 @@ Layout make_layout(const deamoe_config &c) {
     L.zsbuf = take(dpairs * ds * ab);
     L.partial = take((dpairs + (dse ? T : 0)) * h * 4);
   }
-  // fused down stage, batches of at most 16 tokens: routing weights per unit
+  // fused down stage, batches of at most 32 tokens: routing weights per unit
   // and token (and a row of ones), the unit table
-  L.wdense = take((m + n + 1) * kTile * 4);
+  L.wdense = take((m + n + 1) * kChainT * 4);
   L.cunits = take((size_t)kMaxChainUnits * sizeof(ChainUnit));
   L.total = off;
   return L;
@@ -193,23 +193,23 @@ int down_ks_of(const deamoe_config &c, int T) {
 
 
 // Down projections and combine fused into one kernel (the SLICE down stage,
-// the FACTORED department down stage): batches of at most 16 tokens whose
-// active units fit the kernel's unit table.  Its grid is one workgroup per 32
-// rows of y.  SLICE: below kChainMinTiles of them (a hidden size under 4096)
-// it is used up to 4 tokens only, where the separate down stage has too few
-// work items to do better (measured on the 2048-wide layer).  FACTORED: the
-// department down stage is a few long contractions that the split-K stage
-// already streams well; the fused kernel gains only with a grid of at least
-// kChainMinTilesFactored workgroups (measured on the 7168- and 4096-wide
-// Table 1 layers).
+// the FACTORED department down stage): batches whose active units fit the
+// kernel's unit table.  Its grid is one workgroup per 32 rows of y.  SLICE:
+// up to 32 tokens (two token tiles from 17 on); below kChainMinTiles
+// workgroups (a hidden size under 4096) only up to 4 tokens, where the
+// separate down stage has too few work items to do better (measured on the
+// 2048-wide layer).  FACTORED: up to 16 tokens; its department down stage is
+// a few long contractions that the split-K stage already streams well, and
+// the fused kernel gains only with a grid of at least kChainMinTilesFactored
+// workgroups (measured on the 7168- and 4096-wide Table 1 layers).
 #ifndef DEAMOE_CHAIN
 #define DEAMOE_CHAIN 1
 #endif
 constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 192;
 bool use_chain(const deamoe_config &c, int T) {
-  if (!DEAMOE_CHAIN || T > kTile) return false;
+  if (!DEAMOE_CHAIN || T > kChainT) return false;
   const int tiles = c.hidden / (2 * kTile);
-  if (c.form == DEAMOE_FORM_FACTORED && tiles < kChainMinTilesFactored) return false;
+  if (c.form == DEAMOE_FORM_FACTORED && (T > kTile || tiles < kChainMinTilesFactored)) return false;
   if (T > 4 && tiles < kChainMinTiles) return false;
   const int dk = std::min(c.top_k_dept > 0 ? c.top_k_dept : c.top_k, std::min(c.top_k, c.n_depts));
   const bool slice_priv = c.form == DEAMOE_FORM_SLICE && c.d_private > 0;

@@ -1,5 +1,5 @@
-// Down projections of the SLICE form fused with the weighted combine of
-// Eq. 3, for batches of at most 16 tokens.
+// Down projections fused with the weighted combine of Eq. 3, for batches of
+// at most 32 tokens (one or two token tiles of 16).
 //
 // For every active unit u (department, expert, shared expert) the gate/up
 // stage has stored a_{t,u} = SiLU(G_u x_t) * (U_u x_t) for the unit's tokens,
@@ -23,9 +23,9 @@ namespace deamoe {
 
 // One K step of both halves: the step's products start from zero and are
 // added with the per-lane factor f (the token's weight, times the fp8 scale).
-template <int WT>
+template <int WT, int NTT>
 __device__ inline void chain_mma(const u32x4 (&a)[2][4], const u32x4 (&b)[4], float f,
-                                 f32x4 (&acc)[2]) {
+                                 f32x4 (&acc)[2][NTT], int tt) {
 #pragma unroll
   for (int n = 0; n < 2; ++n) {
     f32x4 t = {0.f, 0.f, 0.f, 0.f};
@@ -43,7 +43,7 @@ __device__ inline void chain_mma(const u32x4 (&a)[2][4], const u32x4 (&b)[4], fl
         t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, as_bf16x8(b[m]), t, 0, 0, 0);
       }
     }
-    acc[n] += f * t;
+    acc[n][tt] += f * t;
   }
 }
 
@@ -56,7 +56,7 @@ __device__ inline P *uniform_ptr(P *p) {
   return reinterpret_cast<P *>(((uint64_t)hi << 32) | lo);
 }
 
-template <int WT, int KSC, int PF>
+template <int WT, int NTT, int KSC, int PF>
 __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
   using Tr = WTraits<WT>;
   using LD = WLoad<WT>;
@@ -65,7 +65,7 @@ __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
   constexpr int NB = PF + 1;       // load groups per wave: PF in flight, one multiplied
   constexpr int ASEG = Tr::K_STEP * Tr::A_BYTES;
   constexpr int STAGE = NW * LD::REGION;
-  constexpr int RED = NW * kWave * 16;
+  constexpr int RED = NW * NTT * kWave * 16;
   constexpr int WB = STAGE > RED ? STAGE : RED;
   __shared__ __attribute__((aligned(16))) char s_buf[KSC][WB];
   __shared__ ChainUnit s_u[kMaxChainUnits];
@@ -85,8 +85,12 @@ __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
   const int s_lo = uniform((int)((int64_t)S * wave / KSC));
   const int total = uniform((int)((int64_t)S * (wave + 1) / KSC)) - s_lo;
   char *lds = s_buf[wave];
-  f32x4 acc[NW];
-  acc[0] = acc[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // acc[n][tt]: rows of half n, tokens 16 * tt + (lane % 16)
+  f32x4 acc[NW][NTT];
+#pragma unroll
+  for (int n = 0; n < NW; ++n)
+#pragma unroll
+    for (int tt = 0; tt < NTT; ++tt) acc[n][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (total > 0) {
     // the unit holding step s_lo: the last one whose first step is <= s_lo
     int lo = 0, hi = n_units - 1;
@@ -97,36 +101,43 @@ __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
     int cu = uniform(lo);
     // issue cursor: unit cu, its K step ck of nk; the unit's per-lane state
     int ck = s_lo - uniform(s_u[cu].step0), nk = 0, ldw = 0;
-    const char *w0 = nullptr, *bp = nullptr;
-    const float *sp = nullptr, *pp = nullptr;
-    uint64_t mm = 0;   // lanes whose token is a member of the unit
+    const char *w0 = nullptr, *bp[NTT];
+    const float *sp = nullptr, *pp[NTT];
+    uint64_t mm[NTT];   // per token tile: lanes whose token is a member of the unit
     const uint32_t tmask = T >= 32 ? 0xffffffffu : (1u << T) - 1u;
     auto load_unit = [&](int u) {
       ldw = uniform(s_u[u].K);
       nk = ldw / Tr::K_STEP;
       w0 = static_cast<const char *>(uniform_ptr(s_u[u].w)) + lchunk * 16;
-      const uint32_t m16 = (uint32_t)uniform((int)s_u[u].mask) & tmask & 0xffffu;
-      mm = (uint64_t)m16 * 0x0001000100010001ull;
-      // a member's row is its rank among the members; other lanes read the
-      // first member's row (their weight is zero), so each load touches only
-      // the unit's rows
-      const int rank = (m16 >> j) & 1 ? __popc(m16 & ((1u << j) - 1u)) : 0;
-      bp = static_cast<const char *>(uniform_ptr(s_u[u].in)) + (size_t)rank * ldw * Tr::A_BYTES;
-      pp = uniform_ptr(s_u[u].pw) + j;
+      const uint32_t m32 = (uint32_t)uniform((int)s_u[u].mask) & tmask;
+      const char *in = static_cast<const char *>(uniform_ptr(s_u[u].in));
+      const float *pw = uniform_ptr(s_u[u].pw);
+#pragma unroll
+      for (int tt = 0; tt < NTT; ++tt) {
+        const uint32_t m16 = (m32 >> (kTile * tt)) & 0xffffu;
+        mm[tt] = (uint64_t)m16 * 0x0001000100010001ull;
+        // a member's row is its rank among the members; other lanes read the
+        // first member's row (their weight is zero), so each load touches
+        // only the unit's rows
+        const int tok = kTile * tt + j;
+        const int rank = (m16 >> j) & 1 ? __popc(m32 & ((1u << tok) - 1u)) : 0;
+        bp[tt] = in + (size_t)rank * ldw * Tr::A_BYTES;
+        pp[tt] = pw + tok;
+      }
       if constexpr (WT == WT_FP8)   // the tile's 32 rows lie in one scale row
         sp = uniform_ptr(s_u[u].s) + (size_t)((rt * TR) / 128) * (ldw / 128);
     };
     load_unit(cu);
     // loads past the wave's range read cache-resident data of the first unit
-    const char *dummy = bp + (lane & 15) * 16;
-    const char *dummy_b = bp;
-    const float *dummy_s = sp, *dummy_p = pp;
+    const char *dummy = bp[0] + (lane & 15) * 16;
+    const char *dummy_b = bp[0];
+    const float *dummy_s = sp, *dummy_p = pp[0];
     u32x4 G[NB][NW][LD::NQ];
-    u32x4 B[NB][4];
-    uint64_t MM[NB];
-    float SC[NB], P[NB];
-    auto issue = [&](u32x4(&Gb)[NW][LD::NQ], u32x4(&Bb)[4], uint64_t &mms, float &sc, float &pw,
-                     int v) {
+    u32x4 B[NB][NTT][4];
+    uint64_t MM[NB][NTT];
+    float SC[NB], P[NB][NTT];
+    auto issue = [&](u32x4(&Gb)[NW][LD::NQ], u32x4(&Bb)[NTT][4], uint64_t(&mms)[NTT], float &sc,
+                     float(&pw)[NTT], int v) {
       const bool ok = v < total;
       if (ok && ck == nk) {   // the previous step ended a unit
         ++cu;
@@ -141,12 +152,15 @@ __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
         Gb[0][q] = __builtin_nontemporal_load(gptr(ok ? w0 + woff : dummy));
         Gb[1][q] = __builtin_nontemporal_load(gptr(ok ? w0 + woff + half : dummy));
       }
-      const char *b = ok ? bp + (size_t)ck * ASEG : dummy_b;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) Bb[q] = *gptr(b + b_chunk_offset(g, q));
-      pw = *gfptr(ok ? pp : dummy_p);
+      for (int tt = 0; tt < NTT; ++tt) {
+        const char *b = ok ? bp[tt] + (size_t)ck * ASEG : dummy_b;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) Bb[tt][q] = *gptr(b + b_chunk_offset(g, q));
+        pw[tt] = *gfptr(ok ? pp[tt] : dummy_p);
+        mms[tt] = mm[tt];
+      }
       if constexpr (WT == WT_FP8) sc = *gfptr(ok ? sp + ck : dummy_s);
-      mms = mm;
       if (ok) ++ck;
     };
 #pragma unroll
@@ -159,10 +173,13 @@ __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
         __builtin_amdgcn_sched_barrier(0);
         u32x4 w[NW][4];
         stage_weights<WT, NW>(lds, G[q], w);
-        // tokens outside the unit have weight zero (their operand is a
-        // member's row, so the product is finite)
-        const float f0 = (MM[q] >> lane) & 1 ? P[q] : 0.f;
-        chain_mma<WT>(w, B[q], WT == WT_FP8 ? f0 * SC[q] : f0, acc);
+#pragma unroll
+        for (int tt = 0; tt < NTT; ++tt) {
+          // tokens outside the unit have weight zero (their operand is a
+          // member's row, so the product is finite)
+          const float f0 = (MM[q][tt] >> lane) & 1 ? P[q][tt] : 0.f;
+          chain_mma<WT>(w, B[q][tt], WT == WT_FP8 ? f0 * SC[q] : f0, acc, tt);
+        }
         __builtin_amdgcn_sched_barrier(0);
         if (++v >= total) goto streamed;
       }
@@ -173,39 +190,51 @@ streamed:
   __syncthreads();   // every wave is done with its staging region
   f32x4 *red = reinterpret_cast<f32x4 *>(s_buf[wave]);
   if (wave > 0) {
-    red[lane] = acc[0];
-    red[kWave + lane] = acc[1];
+#pragma unroll
+    for (int n = 0; n < NW; ++n)
+#pragma unroll
+      for (int tt = 0; tt < NTT; ++tt) red[(n * NTT + tt) * kWave + lane] = acc[n][tt];
   }
   __syncthreads();
   if (wave == 0) {
     for (int q = 1; q < KSC; ++q) {
       const f32x4 *r = reinterpret_cast<const f32x4 *>(s_buf[q]);
-      acc[0] += r[lane];
-      acc[1] += r[kWave + lane];
+#pragma unroll
+      for (int n = 0; n < NW; ++n)
+#pragma unroll
+        for (int tt = 0; tt < NTT; ++tt) acc[n][tt] += r[(n * NTT + tt) * kWave + lane];
     }
-    const int row0 = rt * TR + 4 * g;
-    if (j < T) {
-      const size_t off = (size_t)j * R + row0;
-      if (row0 < R) store4(a.y, a.act_f32, off, acc[0], row0 + 3 < R, R - row0);
-      const int row1 = row0 + kTile;
-      if (row1 < R) store4(a.y, a.act_f32, off + kTile, acc[1], row1 + 3 < R, R - row1);
+    const int row0 = rt * TR + 4 * g, row1 = row0 + kTile;
+#pragma unroll
+    for (int tt = 0; tt < NTT; ++tt) {
+      const int tok = kTile * tt + j;
+      if (tok < T) {
+        const size_t off = (size_t)tok * R + row0;
+        if (row0 < R) store4(a.y, a.act_f32, off, acc[0][tt], row0 + 3 < R, R - row0);
+        if (row1 < R) store4(a.y, a.act_f32, off + kTile, acc[1][tt], row1 + 3 < R, R - row1);
+      }
     }
   }
 }
 
-template <int WT>
+template <int WT, int NTT>
 static hipError_t launch_chain_wt(const ChainArgs &a, hipStream_t s) {
   const dim3 grid((a.h + 2 * kTile - 1) / (2 * kTile));
   constexpr int KSC = DEAMOE_CHAIN_WAVES, PF = DEAMOE_CHAIN_PF;
-  hipLaunchKernelGGL((chain_down_kernel<WT, KSC, PF>), grid, dim3(KSC * kWave), 0, s, a);
+  hipLaunchKernelGGL((chain_down_kernel<WT, NTT, KSC, PF>), grid, dim3(KSC * kWave), 0, s, a);
   return hipGetLastError();
+}
+
+template <int WT>
+static hipError_t launch_chain_ntt(const ChainArgs &a, hipStream_t s) {
+  return a.T > kTile ? launch_chain_wt<WT, 2>(a, s) : launch_chain_wt<WT, 1>(a, s);
 }
 
 hipError_t launch_chain(const ChainArgs &a, int wtype, hipStream_t s) {
   switch (wtype) {
-    case WT_F32: return launch_chain_wt<WT_F32>(a, s);
-    case WT_BF16: return launch_chain_wt<WT_BF16>(a, s);
-    default: return launch_chain_wt<WT_FP8>(a, s);
+    case WT_F32: return launch_chain_ntt<WT_F32>(a, s);
+    case WT_BF16: return launch_chain_ntt<WT_BF16>(a, s);
+    default: return launch_chain_ntt<WT_FP8>(a, s);
   }
 }
 

@@ -82,8 +82,8 @@ struct GemmUnit {
   int32_t tpg;              // row tiles per work item (1 unless the K split is 1)
 };
 
-// One unit of the fused down projection and combine of the SLICE form (at
-// most 16 tokens): the [R, K] down matrix w (fp8: block scales s) applied to
+// One unit of the fused down projection and combine (at most 32 tokens): the
+// [R, K] down matrix w (fp8: block scales s) applied to
 // the unit's gate/up outputs `in` ([members, K], one row per member token in
 // ascending token order), each token's product weighted by pw[t].  The K
 // steps of all units form one concatenation.

@@ -61,11 +61,11 @@ struct RouteArgs {
   void *gbuf, *ubuf, *ybuf, *zsbuf;           // FACTORED intermediates (act dtype)
   float *zbuf;                                // FACTORED sigma(A_d^T Y), fp32
   float *partial;                             // [pairs, h] fp32
-  // SLICE at most 16 tokens: down projections fused with the combine
+  // at most kChainT tokens: down projections fused with the combine
   int32_t chain;
   ChainUnit *cunits;                          // units of the fused down stage
-  float *wdense;                              // [m + n + 1][16] routing weight per unit and
-                                              // token (last row: the shared expert's 1)
+  float *wdense;                              // [m + n + 1][kChainT] routing weight per unit
+                                              // and token (last row: ones)
 };
 
 struct CombineArgs {
@@ -76,9 +76,10 @@ struct CombineArgs {
   int32_t T, h, max_slots, act_f32;
 };
 
-// Fused down projection and combine (SLICE form, T <= 16): one workgroup per
-// 32 rows of y.
+// Fused down projection and combine (T <= kChainT): one workgroup per 32
+// rows of y.
 constexpr int kMaxChainUnits = 512;
+constexpr int kChainT = 32;   // tokens; also the row length of the token-weight table
 struct ChainArgs {
   const ChainUnit *units;
   const int32_t *counts;    // [0] = number of units, [1] = K steps of the concatenation

@@ -592,7 +592,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     a.r.topk_ids[t * k + lane] = my_id;
     if (lds.ids) lds.ids[t * k + lane] = my_id;
     a.r.topk_w[t * k + lane] = p;
-    if (a.wdense) a.wdense[(size_t)(a.m + my_id) * kTile + t] = p;
+    if (a.wdense) a.wdense[(size_t)(a.m + my_id) * kChainT + t] = p;
     atomicOr(&s_db[d >> 5], 1u << (d & 31));
   }
   wave_lds_sync();
@@ -617,7 +617,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     a.r.tok_depts[t * k + dpos] = d;
     if (lds.dep) lds.dep[t * k + dpos] = d;
     a.r.tok_dept_w[t * k + dpos] = P;
-    if (a.wdense) a.wdense[(size_t)d * kTile + t] = P;
+    if (a.wdense) a.wdense[(size_t)d * kChainT + t] = P;
     if (a.plan) a.slot_w[(size_t)t * S + dpos] = slice ? P : 1.0f;
   }
   if (lane >= nd && lane < k) {
@@ -837,7 +837,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
     const int gd = tiles_per_item(a.d_s, dr, dk), gp = a.d_p ? tiles_per_item(a.d_p, dr, dk) : 1;
     const int gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
     const int bse = items_of(a.h, gse, dr);
-    // fused down stage (T <= 16): the units' K steps are concatenated in
+    // fused down stage (T <= 32): the units' K steps are concatenated in
     // table order (departments, experts, the shared expert)
     const int sd = a.d_s / kstep, sp = a.d_p / kstep;
     if (tid < m && my_dc > 0) {
@@ -849,7 +849,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                nullptr, a.d_s, a.h, a.h, a.d_s, my_dc, dbeg_a(j, u), EPI_SWIGLU, a.act_f32);
       if (a.chain)
         put_chain(glob(a.cunits) + u, wptr(W.dept_down, j, a.h, a.d_s),
-                  sptr(W.scale[2], j, a.h, a.d_s), ao, a.wdense + (size_t)j * kTile, a.d_s,
+                  sptr(W.scale[2], j, a.h, a.d_s), ao, a.wdense + (size_t)j * kChainT, a.d_s,
                   s_dtok[j * kTW], u * sd);
       else
         put_unit(glob(a.units[1]) + u, wptr(W.dept_down, j, a.h, a.d_s), nullptr,
@@ -870,7 +870,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                a.act_f32);
       if (a.chain)
         put_chain(glob(a.cunits) + u, wptr(W.priv_down, e, a.h, a.d_p),
-                  sptr(W.scale[5], e, a.h, a.d_p), ao, a.wdense + (size_t)(m + e) * kTile, a.d_p,
+                  sptr(W.scale[5], e, a.h, a.d_p), ao, a.wdense + (size_t)(m + e) * kChainT, a.d_p,
                   s_etok[e * kTW], ud * sd + ui * sp);
       else
         put_unit(glob(a.units[1]) + u, wptr(W.priv_down, e, a.h, a.d_p), nullptr,
@@ -879,7 +879,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                  my_ec[q], ebeg_b(e, ui), EPI_STORE, 1, gp);
     }
     // weight 1 of the shared expert: the row after the experts'
-    if (a.chain && tid < kTile) a.wdense[(size_t)(m + n) * kTile + tid] = 1.0f;
+    if (a.chain && tid < kChainT) a.wdense[(size_t)(m + n) * kChainT + tid] = 1.0f;
     if (tid == 0) {
       int units = ud + ue, items_a = tot_a, items_b = tot_b;
       int steps = ud * sd + ue * sp;
@@ -889,7 +889,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                  a.h, a.d_se, T, items_a, EPI_SWIGLU, a.act_f32);
         if (a.chain) {
           put_chain(glob(a.cunits) + units, W.se_down, sptr(W.scale[8], 0, a.h, a.d_se), a.abuf_se,
-                    a.wdense + (size_t)(m + n) * kTile, a.d_se,
+                    a.wdense + (size_t)(m + n) * kChainT, a.d_se,
                     T >= 32 ? 0xffffffffu : (1u << T) - 1u, steps);
           steps += a.d_se / kstep;
         } else {
@@ -923,7 +923,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                a.h, a.h, d, my_dc, dbeg_a(j, u), EPI_SIGMA2, a.act_f32);
       if (a.chain)   // Z already carries the routing weights: unit weight 1
         put_chain(glob(a.cunits) + u, wptr(W.dept_down, j, a.h, d), sptr(W.scale[2], j, a.h, d), zs,
-                  a.wdense + (size_t)(m + n) * kTile, d, s_dtok[j * kTW], u * (d / kstep));
+                  a.wdense + (size_t)(m + n) * kChainT, d, s_dtok[j * kTW], u * (d / kstep));
       else
         put_unit(glob(a.units[3]) + u, wptr(W.dept_down, j, a.h, d), nullptr,
                  sptr(W.scale[2], j, a.h, d), nullptr, zs, zs, nullptr,
@@ -944,7 +944,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                nullptr, yo, yo, nullptr, a.zbuf + (size_t)off * d, nullptr, d, d, d, d,
                my_ec[q], ebeg_b(e, u) - dept_b, EPI_SIGMA, 1, g2);
     }
-    if (a.chain && tid < kTile) a.wdense[(size_t)(m + n) * kTile + tid] = 1.0f;
+    if (a.chain && tid < kChainT) a.wdense[(size_t)(m + n) * kChainT + tid] = 1.0f;
     if (tid == 0) {
       int units0 = ud, items0 = dept_a, units3 = ud, items3 = dept_b;
       int steps = ud * (d / kstep);
@@ -954,7 +954,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                  a.h, a.d_se, T, items0, EPI_SWIGLU, a.act_f32);
         if (a.chain) {
           put_chain(glob(a.cunits) + units3, W.se_down, sptr(W.scale[8], 0, a.h, a.d_se), a.abuf_se,
-                    a.wdense + (size_t)(m + n) * kTile, a.d_se,
+                    a.wdense + (size_t)(m + n) * kChainT, a.d_se,
                     T >= 32 ? 0xffffffffu : (1u << T) - 1u, steps);
           steps += a.d_se / kstep;
         } else {

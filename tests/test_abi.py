@@ -244,10 +244,10 @@ def test_read_probe_library_exports():
 
 
 def test_trace_points():
-    """Stage boundaries of the traced call: batches of at most 16 tokens run
-    the last down stage and the combine as one kernel."""
+    """Stage boundaries of the traced call: small batches run the last down
+    stage and the combine as one kernel."""
     c = cfg_c3()
-    assert [D.deamoe_trace_points(c, T) for T in (1, 4, 16, 17, 64)] == [5, 5, 5, 6, 6]
+    assert [D.deamoe_trace_points(c, T) for T in (1, 4, 16, 17, 32, 33, 64)] == [5, 5, 5, 5, 5, 6, 6]
     s7 = D.make_config(W.PRESETS["7b_bf16"].layer, 64)     # h 2048: fused up to 4 tokens
     assert [D.deamoe_trace_points(s7, T) for T in (1, 4, 5, 16)] == [5, 5, 6, 6]
     f = D.make_config(W.PRESETS["dsv3_factored"].layer, 64)
@@ -257,6 +257,8 @@ def test_trace_points():
     # more active units than the fused kernel's table holds: separate stages
     big = cfg_c3(n_experts=2048, n_depts=64, top_k=32)
     assert [D.deamoe_trace_points(big, T) for T in (8, 16)] == [5, 6]
+    # FACTORED fuses up to 16 tokens only
+    assert D.deamoe_trace_points(D.make_config(W.PRESETS["kimik2_factored"].layer, 64), 32) == 9
     n = C.c_int32(0)
     for T in (0, 65):
         assert D.lib().deamoe_trace_points(C.byref(c), T, C.byref(n)) == D.ERR_INVALID

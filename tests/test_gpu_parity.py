@@ -75,14 +75,15 @@ def test_small_variants(variant):
 
 @pytest.mark.parametrize("variant", ["f32_t13_se", "f32_t16_no_private", "f32_t7_group_limited",
                                      "bf16_t16_sigmoid", "fp8_t11_se", "f32_baseline_t9",
-                                     "factored_t13_se_rmsnorm", "factored_fp8_t16"])
+                                     "factored_t13_se_rmsnorm", "factored_fp8_t16",
+                                     "f32_t29_se", "fp8_t32", "bf16_t17_group_limited"])
 def test_fused_down_combine(variant):
-    """The last down stage and the combine in one kernel (at most 16 tokens,
-    hidden 4096 = 128 tiles of 32 rows; FACTORED 6144 = 192 tiles): ragged
-    batches, a shared expert, no private part, a group-limited gate, bf16 and
-    fp8 weights (32 scale rows, 4 scale blocks per department contraction),
-    the vanilla layer, and the FACTORED W_d^T stage (RMSNorm sigma, fp8);
-    every output checked."""
+    """The last down stage and the combine in one kernel (SLICE up to 32
+    tokens at hidden 4096 = 128 tiles of 32 rows; FACTORED up to 16 at 6144 =
+    192 tiles): ragged batches over one and two token tiles, a shared expert,
+    no private part, a group-limited gate, bf16 and fp8 weights (32 scale
+    rows, 4 scale blocks per department contraction), the vanilla layer, and
+    the FACTORED W_d^T stage (RMSNorm sigma, fp8); every output checked."""
     base = small(hidden=4096)
     baseline = False
     if variant == "f32_t13_se":
@@ -100,6 +101,13 @@ def test_fused_down_combine(variant):
     elif variant == "f32_baseline_t9":
         cfg = base.replace(name="small_baseline", n_depts=16, d_shared=576, d_private=0)
         case, baseline = Case(cfg, 9, seed=46), True
+    elif variant == "f32_t29_se":   # two token tiles, ragged
+        case = Case(base.replace(d_shared_expert=192), 29, seed=49)
+    elif variant == "fp8_t32":
+        case = Case(base.replace(w_dtype="fp8", act_dtype="bf16", d_private=256), 32, seed=50)
+    elif variant == "bf16_t17_group_limited":
+        case = Case(base.replace(w_dtype="bf16", act_dtype="bf16", d_private=128, n_experts=64,
+                                 n_depts=8, top_k=6, top_k_dept=3), 17, seed=51)
     elif variant == "factored_t13_se_rmsnorm":   # W_d^T Z with the weights already in Z
         case = Case(base.replace(hidden=6144, form="factored", d_shared=256, d_private=0,
                                  d_shared_expert=128, sigma="rmsnorm"), 13, seed=47)
@@ -147,7 +155,7 @@ def test_7b_bf16_baseline():
 
 # ------------------------------------------------------------ full size, sampled
 
-@pytest.mark.parametrize("T", [1, 16, 64, 128])
+@pytest.mark.parametrize("T", [1, 16, 32, 64, 128])
 def test_dsv3_bf16(T):
     case = Case(P["dsv3_bf16"].layer, T, seed=50 + T, max_tokens=128 if T > 64 else None)
     check_case(case, tokens=sample_tokens(T))
