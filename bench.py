@@ -36,8 +36,8 @@ HBM_PEAK_GBPS = 8000.0
 # FETCH_SIZE and WRITE_SIZE passes scaled by what the same counters read for a
 # 1 GiB device copy (x2.0 and x1.0).  Valid only for the library sources they
 # were taken on: the digest below covers them, and a mismatch reports null.
-TRAFFIC_BYTES = 2341126963
-TRAFFIC_SOURCES_SHA256 = "281a17ae496177be6bb73973ae5526b95d3b7dc95976a15ca8278e4c6febaace"
+TRAFFIC_BYTES = 2341126995
+TRAFFIC_SOURCES_SHA256 = "a6f289ec48cdccc5776727b4a4783511f55ff19d25b7793440409ff64999cf85"
 
 
 def library_sources_digest() -> str:
