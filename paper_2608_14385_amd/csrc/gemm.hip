@@ -10,7 +10,7 @@ namespace deamoe {
 constexpr int kMaxUnitsCached = 4096;
 
 template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR>
-__global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
+__device__ __attribute__((always_inline)) void grouped_gemm_body(const GemmStage &st) {
   using Run = TileRunner<WT, NW, NTT, KS, SPLIT, PAIR>;
   __shared__ typename Run::Smem sm;
   __shared__ int32_t s_begin[kMaxUnitsCached];
@@ -37,6 +37,22 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
   }
 }
 
+template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR>
+__global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
+  grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR>(st);
+}
+
+// Two-matrix stages with split token operands (the FACTORED private gate/up)
+// hold both operands' prefetch in registers: left alone the compiler takes
+// 166 registers, two waves per SIMD.  With one token tile, three (168
+// registers, no spills) keep the 640 workgroups of a one-token step resident
+// in one round.
+template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+void grouped_gemm_split_kernel(GemmStage st) {
+  grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR>(st);
+}
+
 // mode: GemmMode; row pairs exist for NTT <= 2 only (the host picks them so)
 template <int WT, int NW, int NTT, int KS>
 static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int grid_cap,
@@ -46,8 +62,12 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
   grid = grid < 1 ? 1 : (grid > grid_cap ? grid_cap : grid);
   if constexpr (NW == 2) {
     if (mode == 1) {
-      hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, true, false>), dim3(grid), dim3(256),
-                         0, s, st);
+      if constexpr (NTT == 1 && KS > 1)
+        hipLaunchKernelGGL((grouped_gemm_split_kernel<WT, NW, NTT, KS, true, false>), dim3(grid),
+                           dim3(256), 0, s, st);
+      else   // two token tiles (or no K split) would spill at three waves per SIMD
+        hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, true, false>), dim3(grid),
+                           dim3(256), 0, s, st);
       return hipGetLastError();
     }
     if (mode == 2) {

@@ -592,7 +592,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     a.r.topk_ids[t * k + lane] = my_id;
     if (lds.ids) lds.ids[t * k + lane] = my_id;
     a.r.topk_w[t * k + lane] = p;
-    if (a.wdense) a.wdense[(size_t)(a.m + my_id) * kChainT + t] = p;
+    if (a.wdense) glob(a.wdense)[(size_t)(a.m + my_id) * kChainT + t] = p;
     atomicOr(&s_db[d >> 5], 1u << (d & 31));
   }
   wave_lds_sync();
@@ -617,7 +617,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     a.r.tok_depts[t * k + dpos] = d;
     if (lds.dep) lds.dep[t * k + dpos] = d;
     a.r.tok_dept_w[t * k + dpos] = P;
-    if (a.wdense) a.wdense[(size_t)d * kChainT + t] = P;
+    if (a.wdense) glob(a.wdense)[(size_t)d * kChainT + t] = P;
     if (a.plan) a.slot_w[(size_t)t * S + dpos] = slice ? P : 1.0f;
   }
   if (lane >= nd && lane < k) {
@@ -879,7 +879,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                  my_ec[q], ebeg_b(e, ui), EPI_STORE, 1, gp);
     }
     // weight 1 of the shared expert: the row after the experts'
-    if (a.chain && tid < kChainT) a.wdense[(size_t)(m + n) * kChainT + tid] = 1.0f;
+    if (a.chain && tid < kChainT) glob(a.wdense)[(size_t)(m + n) * kChainT + tid] = 1.0f;
     if (tid == 0) {
       int units = ud + ue, items_a = tot_a, items_b = tot_b;
       int steps = ud * sd + ue * sp;
@@ -944,7 +944,7 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
                nullptr, yo, yo, nullptr, a.zbuf + (size_t)off * d, nullptr, d, d, d, d,
                my_ec[q], ebeg_b(e, u) - dept_b, EPI_SIGMA, 1, g2);
     }
-    if (a.chain && tid < kChainT) a.wdense[(size_t)(m + n) * kChainT + tid] = 1.0f;
+    if (a.chain && tid < kChainT) glob(a.wdense)[(size_t)(m + n) * kChainT + tid] = 1.0f;
     if (tid == 0) {
       int units0 = ud, items0 = dept_a, units3 = ud, items3 = dept_b;
       int steps = ud * (d / kstep);
