@@ -424,7 +424,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
   } else {
     const int d = c.d_shared;
     const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, t0 * groups, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, DEAMOE_KS_FGU, t0 * groups,
+                                   kGridCap, s));
     if (c.sigma == DEAMOE_SIGMA_RMSNORM) {   // timed with stage 0
       RowNormArgs na;
       na.counts = pc;

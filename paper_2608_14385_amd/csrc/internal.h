@@ -31,6 +31,10 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #ifndef DEAMOE_SDOWN_KS2_T
 #define DEAMOE_SDOWN_KS2_T 2
 #endif
+// K split of the FACTORED department gate/up stage (W_g x, W_u x).
+#ifndef DEAMOE_KS_FGU
+#define DEAMOE_KS_FGU 4
+#endif
 // K split of the FACTORED private gate/up stage (A_g G, A_u U).
 #ifndef DEAMOE_KS_FPRIV
 #define DEAMOE_KS_FPRIV 2
