@@ -42,16 +42,21 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
   grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR>(st);
 }
 
-// Two-matrix stages with split token operands (the FACTORED private gate/up)
-// hold both operands' prefetch in registers: left alone the compiler takes
-// 166 registers, two waves per SIMD.  With one token tile, three (168
-// registers, no spills) keep the 640 workgroups of a one-token step resident
-// in one round.
+// The same at three waves per SIMD (at most 168 registers).  Left alone the
+// compiler gives two-matrix stages with split token operands (the FACTORED
+// private gate/up) 166 registers, two waves per SIMD; with one token tile,
+// three (no spills) keep the 640 workgroups of a one-token step resident in
+// one round.
 template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
-void grouped_gemm_split_kernel(GemmStage st) {
+void grouped_gemm_occ3_kernel(GemmStage st) {
   grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR>(st);
 }
+
+// fp8 stages with two token tiles also fit three waves without spilling
+// (bf16 ones would spill, which costs far more than the occupancy gains).
+template <int WT, int NTT>
+constexpr bool occ3_two_tiles() { return NTT == 2 && WT == WT_FP8; }
 
 // mode: GemmMode; row pairs exist for NTT <= 2 only (the host picks them so)
 template <int WT, int NW, int NTT, int KS>
@@ -63,7 +68,7 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
   if constexpr (NW == 2) {
     if (mode == 1) {
       if constexpr (NTT == 1 && KS > 1)
-        hipLaunchKernelGGL((grouped_gemm_split_kernel<WT, NW, NTT, KS, true, false>), dim3(grid),
+        hipLaunchKernelGGL((grouped_gemm_occ3_kernel<WT, NW, NTT, KS, true, false>), dim3(grid),
                            dim3(256), 0, s, st);
       else   // two token tiles (or no K split) would spill at three waves per SIMD
         hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, true, false>), dim3(grid),
@@ -72,15 +77,23 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
     }
     if (mode == 2) {
       if constexpr (NTT <= 2) {   // row pairs are built for up to two token tiles
-        hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false, true>), dim3(grid),
-                           dim3(256), 0, s, st);
+        if constexpr (occ3_two_tiles<WT, NTT>())
+          hipLaunchKernelGGL((grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, true>), dim3(grid),
+                             dim3(256), 0, s, st);
+        else
+          hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false, true>), dim3(grid),
+                             dim3(256), 0, s, st);
         return hipGetLastError();
       }
       return hipErrorInvalidValue;
     }
   }
-  hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false, false>), dim3(grid), dim3(256), 0,
-                     s, st);
+  if constexpr (NW == 2 && occ3_two_tiles<WT, NTT>())
+    hipLaunchKernelGGL((grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, false>), dim3(grid),
+                       dim3(256), 0, s, st);
+  else
+    hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false, false>), dim3(grid),
+                       dim3(256), 0, s, st);
   return hipGetLastError();
 }
 
