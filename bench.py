@@ -114,12 +114,14 @@ class Hip:
 class LayerRun:
     """R weight copies, token batches and workspace of one layer on the GPU."""
 
-    def __init__(self, cfg, max_tokens: int, copies: int, baseline: bool, seed=0):
+    def __init__(self, cfg, max_tokens: int, copies: int, baseline: bool, seed=0, bias=None):
         import torch
         from paper_2608_14385_amd import deamoe as D
         from paper_2608_14385_amd import workloads as W
         self.D, self.W, self.torch = D, W, torch
         self.cfg, self.baseline = cfg, baseline
+        self.bias = bias   # optional fp32 router bias [n] on the device (skewed routing)
+        self.bias_ptr = bias.data_ptr() if bias is not None else None
         t0 = time.time()
         w0 = W.make_weights(cfg, seed, device="cuda")
         self.copies = [w0] + [{k: v.clone() for k, v in w0.items()} for _ in range(copies - 1)]
@@ -143,9 +145,11 @@ class LayerRun:
         self.bytes = []
         for x in self.xs:
             rt = self.D.Routing.alloc(self.cfg, T)
-            self.D.deamoe_layer_forward(self.c, x, self.structs[0], self.y, self.ws, routing=rt) \
+            self.D.deamoe_layer_forward(self.c, x, self.structs[0], self.y, self.ws,
+                                        router_bias=self.bias, routing=rt) \
                 if not self.baseline else \
-                self.D.deamoe_baseline_forward(self.c, x, self.structs[0], self.y, self.ws, routing=rt)
+                self.D.deamoe_baseline_forward(self.c, x, self.structs[0], self.y, self.ws,
+                                               router_bias=self.bias, routing=rt)
             h = rt.host()
             wb, tb = self.D.deamoe_loaded_bytes(self.c, T, h["dept_count"], h["exp_count"])
             self.bytes.append((wb, tb, h["dept_count"], h["exp_count"]))
@@ -155,13 +159,22 @@ class LayerRun:
         x = self.xs[i % len(self.xs)]
         W = self.structs[i % len(self.structs)]
         s = self.torch.cuda.current_stream().cuda_stream
-        rc = self.fn(C.byref(self.c), self.T, x.data_ptr(), C.byref(W), None, None, None,
+        rc = self.fn(C.byref(self.c), self.T, x.data_ptr(), C.byref(W), None, self.bias_ptr, None,
                      self.y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), s)
         if rc:
             raise RuntimeError(f"layer call failed: {self.D.status_string(rc)}")
 
     def step_bytes(self, i: int) -> int:
         return self.bytes[i % len(self.xs)][1]
+
+    def routing_stats(self) -> dict:
+        """Realised routing of the token batches (mean over batches): tokens
+        of the busiest department, departments and experts touched."""
+        dc = [np.asarray(b[2]) for b in self.bytes]
+        ec = [np.asarray(b[3]) for b in self.bytes]
+        return {"max_dept_tokens": round(float(np.mean([d.max() for d in dc])), 2),
+                "departments": round(float(np.mean([(d > 0).sum() for d in dc])), 2),
+                "experts": round(float(np.mean([(e > 0).sum() for e in ec])), 2)}
 
     def time_direct(self, steps: int, warmup: int) -> float:
         torch = self.torch
@@ -231,7 +244,8 @@ class LayerRun:
             W = self.structs[i % len(self.structs)]
             arr = (C.c_void_p * n_ev)(*evs[i])
             s = torch.cuda.current_stream().cuda_stream
-            rc = self.traced(C.byref(self.c), self.T, x.data_ptr(), C.byref(W), None, None, None,
+            rc = self.traced(C.byref(self.c), self.T, x.data_ptr(), C.byref(W), None, self.bias_ptr,
+                             None,
                              self.y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), s, arr, n_ev)
             assert rc == 0, rc
         torch.cuda.synchronize()
@@ -371,12 +385,13 @@ def cpu_single_core(run: LayerRun, T: int, hw: dict, min_seconds: float = 3.0) -
     (its cost is per token and expert), scaled to whole steps."""
     import oracle
     threads = oracle.num_threads()
+    bias = run.bias.cpu() if run.bias is not None else None
     oracle.set_num_threads(1)
     try:
         done, t0 = 0, time.perf_counter()
         while done < 4 * T and (done == 0 or time.perf_counter() - t0 < min_seconds):
             i, t = (done // T) % len(run.xs), done % T
-            oracle.layer(run.cfg, run.xs[i].cpu(), hw, tokens=[t])
+            oracle.layer(run.cfg, run.xs[i].cpu(), hw, bias=bias, tokens=[t])
             done += 1
         dt = time.perf_counter() - t0
     finally:
@@ -421,10 +436,11 @@ def cpu_baseline(run: LayerRun, T: int, min_seconds: float = 10.0) -> dict:
     import oracle
     threads = oracle.num_threads()
     hw = {k: v.cpu() for k, v in run.copies[0].items()}
+    bias = run.bias.cpu() if run.bias is not None else None
     done, nbytes, t0 = 0, 0, time.perf_counter()
     while done < 16 and (done == 0 or time.perf_counter() - t0 < min_seconds):
         i = done % len(run.xs)
-        oracle.layer(run.cfg, run.xs[i].cpu(), hw)
+        oracle.layer(run.cfg, run.xs[i].cpu(), hw, bias=bias)
         nbytes += run.step_bytes(i)
         done += 1
     dt = time.perf_counter() - t0
@@ -462,7 +478,10 @@ def main():
 
     layer_bytes = sum(math.prod(s) for s in W.weight_shapes(cfg).values()) * \
         {"f32": 4, "bf16": 2, "fp8": 1}[cfg.w_dtype]
-    run = LayerRun(cfg, max_T, copies_for(layer_bytes), baseline=False)
+    # skewed routing: one per-expert router bias for both layers, so that the
+    # vanilla layer sees the same logits distribution
+    bias = W.make_zipf_bias(cfg).cuda() if wl.routing == "zipf_bias" else None
+    run = LayerRun(cfg, max_T, copies_for(layer_bytes), baseline=False, bias=bias)
     T = args.batch
     run.set_batch(T)
     step_bytes = [run.step_bytes(i) for i in range(args.steps)]
@@ -473,12 +492,16 @@ def main():
               "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
               "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.w_dtype,
               "data": "synthetic (seeded gaussian weights and tokens, resident in HBM)"}
+    if cfg.form == "slice":
+        shape = f"department slice {cfg.d_shared} + private slice {cfg.d_private}"
+    else:
+        shape = f"FACTORED (Eq. 4), d={cfg.d_shared}, top-{cfg.top_k_dept} departments"
     result["config"] = {
-        "workload": f"{cfg.name}: DeepSeek-V3-shaped DeaMoE layer, SLICE form, h={cfg.hidden}, "
-                    f"{cfg.n_experts} experts in {cfg.n_depts} departments, top-{cfg.top_k} "
-                    f"{cfg.score}, department slice {cfg.d_shared} + private slice {cfg.d_private}, "
-                    f"{cfg.w_dtype} weights" if cfg.name.startswith("dsv3") else cfg.name,
+        "workload": f"{cfg.name}: DeaMoE layer, h={cfg.hidden}, {cfg.n_experts} experts in "
+                    f"{cfg.n_depts} departments, top-{cfg.top_k} {cfg.score}, {shape}, "
+                    f"{cfg.w_dtype} weights",
         "batch_tokens": T, "weight_copies": len(run.copies), "token_batches": len(run.xs),
+        "routing": wl.routing, "realised_routing": run.routing_stats(),
         "timing": "direct launches on one stream, torch.cuda events around all steps"}
     result["latency_us"] = round(ms * 1e3, 2)
     each = run.time_each(args.steps, 5) * 1e3
@@ -520,7 +543,7 @@ def main():
     if not args.no_baseline:
         bbytes = sum(math.prod(s) for s in W.weight_shapes(bcfg).values()) * \
             {"f32": 4, "bf16": 2, "fp8": 1}[bcfg.w_dtype]
-        brun = LayerRun(bcfg, max_T, copies_for(bbytes), baseline=True)
+        brun = LayerRun(bcfg, max_T, copies_for(bbytes), baseline=True, bias=bias)
     for Tb in sweep:
         row = {"batch": Tb}
         for name, r in (("deamoe", run), ("vanilla", brun)):
@@ -531,7 +554,7 @@ def main():
             m = r.time_direct(k, max(5, k // 5))
             by = float(np.mean([r.step_bytes(i) for i in range(k)]))
             row[name] = {"latency_us": round(m * 1e3, 2), "bytes": int(by),
-                         "GBps": round(by / (m * 1e-3) / 1e9, 1)}
+                         "GBps": round(by / (m * 1e-3) / 1e9, 1), "routing": r.routing_stats()}
             if not args.no_graph:
                 gm = r.time_graph(k, 8)
                 row[name]["graph_latency_us"] = round(gm * 1e3, 2)

@@ -380,8 +380,8 @@ __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int tok0, int si
 // along K (interleaved K steps, partial tiles summed in a fixed order
 // through LDS; work items of one tile), or with KS == 1 one work item of
 // `tpg` tiles per wave.  A unit with more than 16 * NTT tokens has one work
-// item per token group of 16 * NTT tokens and tile item (item = tile item
-// * groups + group), so consecutive items share the weight rows.
+// item per token group of 16 * NTT tokens and tile item; the items of one
+// tile item are 8 * TPB apart, in workgroups on the same XCD.
 // SPLIT: the two matrices read different token operands (in0 / in1).
 #ifndef DEAMOE_PF_NW1
 #define DEAMOE_PF_NW1 1
@@ -415,12 +415,31 @@ struct TileRunner {
     if (active) {
       constexpr int GT = kTile * NTT;   // tokens of a group
       const int groups = (uniform(U->ntok) + GT - 1) / GT;
-      if (groups > 1) {
-        tok0 = (item % groups) * GT;
-        item = item / groups;
-      }
       const int tpg = KS == 1 ? uniform(U->tpg) : 1;
       const int ntiles = (uniform(U->R) + TR - 1) / TR;
+      if (groups > 1) {
+        // The token groups of one tile item stream the same weight rows.
+        // Items S apart run in workgroups 8 apart, which the dispatcher puts
+        // on the same XCD, so a tile's groups are numbered S apart (blocks of
+        // S tile items, group-major inside a block; the last block holds the
+        // r remaining tile items): the later groups' reads find the rows in
+        // that XCD's L2.
+        constexpr int S = 8 * TPB;
+        const int nti = (ntiles + tpg - 1) / tpg;   // tile items of the unit
+        const int full = nti / S;
+        int g, ti;
+        if (item < full * S * groups) {
+          const int b = item / (S * groups), w = item - b * (S * groups);
+          g = w / S;
+          ti = b * S + (w - g * S);
+        } else {
+          const int r = nti - full * S, w = item - full * S * groups;
+          g = w / r;
+          ti = full * S + (w - g * r);
+        }
+        tok0 = uniform(g) * GT;
+        item = uniform(ti);
+      }
       rt0 = item * tpg;
       nsub = min(tpg, ntiles - rt0);
       auto done = [&](int rt, const f32x4 (&a)[NW][NTT]) {
