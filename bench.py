@@ -36,8 +36,8 @@ HBM_PEAK_GBPS = 8000.0
 # FETCH_SIZE and WRITE_SIZE passes scaled by what the same counters read for a
 # 1 GiB device copy (x2.0 and x1.0).  Valid only for the library sources they
 # were taken on: the digest below covers them, and a mismatch reports null.
-TRAFFIC_BYTES = 2341116710
-TRAFFIC_SOURCES_SHA256 = "f0c2e01df693a0f7dae346027c5a3b9f4b14bc34da0da910a1113226aeca3929"
+TRAFFIC_BYTES = 2341114701
+TRAFFIC_SOURCES_SHA256 = "86360348c45547a6ac6e381d27808e9cb1d0084df3bc91f7171d584a5b960a7d"
 
 
 def library_sources_digest() -> str:
