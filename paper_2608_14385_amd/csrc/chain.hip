@@ -15,7 +15,9 @@
 // one long run of weight rows; each K step's product is added to the
 // accumulator with the lane's token weight (times the fp8 block scale), and
 // the partial tiles are summed through LDS in wave order and rounded once.
-// No fp32 partial rows and no combine launch.
+// No fp32 partial rows and no combine launch.  The FACTORED department down
+// projections (W_d^T Z) are the same product over the departments, with the
+// routing weights already inside Z and unit weights here.
 #include "gemm_tile.h"
 #include "launch.h"
 
