@@ -191,7 +191,7 @@ __device__ inline void stage_weights(char *lds, const u32x4 (&Gb)[NW][WLoad<WT>:
 // row instead of weights, so every iteration issues the same loads.
 // `done(rt, acc)` is called (and acc cleared) after the last K step of
 // each tile when nsub > 1; with nsub == 1 the caller finishes the tile.
-template <int WT, int NW, int NTT, bool SPLIT, int PF, bool PAIR, class Done>
+template <int WT, int NW, int NTT, bool SPLIT, int PF, bool PAIR, bool NT, class Done>
 __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, int ks, int tok0,
                                  char *lds, f32x4 (&acc)[NW][NTT], Done done) {
   static_assert(!PAIR || (NW == 2 && !SPLIT), "a row pair is two tiles of one matrix");
@@ -256,7 +256,8 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
       const size_t woff = (size_t)row * ldw * Tr::W_BYTES + (size_t)kstep * LD::WSEG;
 #pragma unroll
       for (int n = 0; n < NW; ++n)
-        Gb[n][q] = __builtin_nontemporal_load(gptr(ok ? (n ? w1 : w0) + woff : dummy));
+        Gb[n][q] = NT ? __builtin_nontemporal_load(gptr(ok ? (n ? w1 : w0) + woff : dummy))
+                      : *gptr(ok ? (n ? w1 : w0) + woff : dummy);
     }
     load_b<WT, NTT, SPLIT>(Bb, bp0, bp1, ntt, (size_t)kstep * ASEG, g);
     if constexpr (WT == WT_FP8)   // a row pair lies in one scale row
@@ -445,8 +446,16 @@ struct TileRunner {
       auto done = [&](int rt, const f32x4 (&a)[NW][NTT]) {
         tile_epilogue<NW, NTT, PAIR>(*U, rt, tok0, sigma, a);
       };
-      tile_loop<WT, NW, NTT, SPLIT, PF, PAIR>(*U, rt0, nsub, kp, KS, tok0, sm.buf[wave], acc,
-                                              done);
+      // A unit with several token groups streams its weight rows once per
+      // group: those loads stay in the caches for the other groups (the
+      // groups of a tile item run on one XCD at about the same time); every
+      // other weight row is read once and streams past them.
+      if (groups > 1)
+        tile_loop<WT, NW, NTT, SPLIT, PF, PAIR, false>(*U, rt0, nsub, kp, KS, tok0, sm.buf[wave],
+                                                       acc, done);
+      else
+        tile_loop<WT, NW, NTT, SPLIT, PF, PAIR, true>(*U, rt0, nsub, kp, KS, tok0, sm.buf[wave],
+                                                      acc, done);
     }
     if constexpr (KS > 1) {
       f32x4 *red = reinterpret_cast<f32x4 *>(sm.buf[wave]);
