@@ -171,10 +171,16 @@ int ntt_of(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
 
 // Token tiles per wave in the expert stages: at most 2, so that row pairs
 // and two-matrix tiles keep their accumulators in registers.  A unit with
-// more tokens than one wave holds gets one work item per token group.
-int wave_ntt_of(int T) { return T <= kTile ? 1 : 2; }
-int token_groups_max(int T) {
-  const int gt = kTile * wave_ntt_of(T);
+// more tokens than one wave holds gets one work item per token group.  The
+// FACTORED stages keep one tile at every batch: its private gate/up then
+// runs at three waves per SIMD, which outweighs streaming the rows of a
+// unit with more than 16 tokens once per group.
+int wave_ntt_of(const deamoe_config &c, int T) {
+  if (DEAMOE_FACTORED_NTT1 && c.form == DEAMOE_FORM_FACTORED) return 1;
+  return T <= kTile ? 1 : 2;
+}
+int token_groups_max(const deamoe_config &c, int T) {
+  const int gt = kTile * wave_ntt_of(c, T);
   return (T + gt - 1) / gt;
 }
 
@@ -208,6 +214,8 @@ int down_ks_of(const deamoe_config &c, int T) {
 constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 192;
 bool use_chain(const deamoe_config &c, int T) {
   if (!DEAMOE_CHAIN || T > kChainT) return false;
+  // the plan builds the fused kernel's units for one token group only
+  if (token_groups_max(c, T) > 1) return false;
   const int tiles = c.hidden / (2 * kTile);
   if (c.form == DEAMOE_FORM_FACTORED && (T > kTile || tiles < kChainMinTilesFactored)) return false;
   if (T > 4 && tiles < kChainMinTiles) return false;
@@ -284,7 +292,7 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
   a.plan = plan;
   a.down_rows = down_rows_of(T);
   a.down_ks = down_ks_of(c, T);
-  a.wave_tokens = kTile * wave_ntt_of(T);
+  a.wave_tokens = kTile * wave_ntt_of(c, T);
   a.part = at<float>(ws, L.part);
   a.kc = L.kc;
   a.ldp = 64 * route_ns(c.n_experts);
@@ -354,12 +362,12 @@ int tiles_bound(int units_max, int R, int rows = kTile) {
 }
 
 // Launch of a down-projection stage.
-hipError_t launch_down(const GemmStage &st, int wt, int T, int ks, int units_max, int R, int cap,
-                       hipStream_t s) {
+hipError_t launch_down(const GemmStage &st, int wt, int T, int ntt, int groups, int ks,
+                       int units_max, int R, int cap, hipStream_t s) {
   const int rows = down_rows_of(T);
   const bool pair = rows == 2 * kTile;
-  return launch_grouped_gemm(st, wt, pair ? 2 : 1, pair ? GEMM_PAIR : GEMM_PLAIN, wave_ntt_of(T),
-                             ks, tiles_bound(units_max, R, rows) * token_groups_max(T), cap, s);
+  return launch_grouped_gemm(st, wt, pair ? 2 : 1, pair ? GEMM_PAIR : GEMM_PLAIN, ntt, ks,
+                             tiles_bound(units_max, R, rows) * groups, cap, s);
 }
 
 constexpr int kGridCap = 8192;   // 256 CUs x 32 workgroups
@@ -387,7 +395,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
                      slice ? PLAN_SLICE : PLAN_FACTORED, w, ev, s);
   if (rc) return rc;
   const int wt = c.w_dtype == DEAMOE_F32 ? WT_F32 : c.w_dtype == DEAMOE_BF16 ? WT_BF16 : WT_FP8;
-  const int ntt = wave_ntt_of(T), groups = token_groups_max(T);
+  const int ntt = wave_ntt_of(c, T), groups = token_groups_max(c, T);
   const PlanCounts *pc = at<PlanCounts>(ws, L.counts);
   auto stage = [&](int i) {
     GemmStage st;
@@ -419,7 +427,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
       return DEAMOE_OK;
     }
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
-    DEAMOE_TRY(launch_down(stage(1), wt, T, down_ks_of(c, T), units, c.hidden, kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(1), wt, T, ntt, groups, down_ks_of(c, T), units, c.hidden,
+                           kGridCap, s));
     DEAMOE_TRY(ev.mark());
   } else {
     const int d = c.d_shared;
@@ -439,7 +448,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, DEAMOE_KS_FPRIV,
                                    tiles_bound(act_exps, d) * groups, kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_down(stage(2), wt, T, down_ks_of(c, T), act_exps, d, kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(2), wt, T, ntt, groups, down_ks_of(c, T), act_exps, d,
+                           kGridCap, s));
     DEAMOE_TRY(ev.mark());
     ZsumArgs za;
     za.counts = pc;
@@ -470,8 +480,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
       DEAMOE_TRY(ev.mark());
       return DEAMOE_OK;
     }
-    DEAMOE_TRY(launch_down(stage(3), wt, T, down_ks_of(c, T), act_depts + se, c.hidden, kGridCap,
-                           s));
+    DEAMOE_TRY(launch_down(stage(3), wt, T, ntt, groups, down_ks_of(c, T), act_depts + se,
+                           c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
   }
   CombineArgs ca;

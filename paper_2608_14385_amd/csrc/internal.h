@@ -50,6 +50,9 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Fused SLICE down stage: waves per workgroup (each streams one contiguous
 // range of the concatenated K steps) and load groups in flight per wave.
+#ifndef DEAMOE_FACTORED_NTT1
+#define DEAMOE_FACTORED_NTT1 1   // FACTORED stages: one token tile per wave at every batch
+#endif
 #ifndef DEAMOE_CHAIN_WAVES
 #define DEAMOE_CHAIN_WAVES 8
 #endif
