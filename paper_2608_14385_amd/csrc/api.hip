@@ -194,7 +194,9 @@ int down_rows_of(int) { return DEAMOE_DOWN_PAIR ? 2 * kTile : kTile; }
 // too few tiles to occupy the waves.
 int down_ks_of(const deamoe_config &c, int T) {
   if (c.form == DEAMOE_FORM_SLICE) return T <= DEAMOE_SDOWN_KS2_T ? 2 : DEAMOE_KS_DOWN;
-  return T <= DEAMOE_FDOWN_KS4_T ? 4 : T <= DEAMOE_FDOWN_KS2_T ? 2 : 1;
+  if (T <= DEAMOE_FDOWN_KS4_T) return 4;
+  const bool wide = c.hidden >= 4096;
+  return T <= DEAMOE_FDOWN_KS2_T || (wide && T <= DEAMOE_FDOWN_KS2_WIDE_T) ? 2 : 1;
 }
 
 

@@ -40,19 +40,24 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define DEAMOE_KS_FPRIV 2
 #endif
 // FACTORED down-projection stages split K four ways up to this many tokens,
-// two ways up to the next.
+// two ways up to the next (up to the third for hidden sizes of 4096 and up).
 #ifndef DEAMOE_FDOWN_KS4_T
 #define DEAMOE_FDOWN_KS4_T 8
 #endif
 #ifndef DEAMOE_FDOWN_KS2_T
-#define DEAMOE_FDOWN_KS2_T 16
+#define DEAMOE_FDOWN_KS2_T 32
+#endif
+#ifndef DEAMOE_FDOWN_KS2_WIDE_T
+#define DEAMOE_FDOWN_KS2_WIDE_T 64
 #endif
 
+// FACTORED stages take one token tile per wave at every batch (0: two tiles
+// from 17 tokens on, as SLICE).
+#ifndef DEAMOE_FACTORED_NTT1
+#define DEAMOE_FACTORED_NTT1 1
+#endif
 // Fused SLICE down stage: waves per workgroup (each streams one contiguous
 // range of the concatenated K steps) and load groups in flight per wave.
-#ifndef DEAMOE_FACTORED_NTT1
-#define DEAMOE_FACTORED_NTT1 1   // FACTORED stages: one token tile per wave at every batch
-#endif
 #ifndef DEAMOE_CHAIN_WAVES
 #define DEAMOE_CHAIN_WAVES 8
 #endif

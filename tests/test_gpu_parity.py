@@ -203,17 +203,18 @@ def test_fp8_small(variant):
 
 @pytest.mark.parametrize("T", [1, 16, 64])
 def test_dsv3_factored(T):
-    """64 tokens: departments with more than one 32-token group (item prefixes
-    from block scans in the plan)."""
+    """64 tokens: departments with several 16-token groups (item prefixes from
+    block scans in the plan) and down stages split over two waves."""
     case = Case(P["dsv3_factored"].layer, T, seed=80 + T)
     check_case(case, tokens=sample_tokens(T, 2))
 
 
 @pytest.mark.parametrize("preset", ["qwen3_factored", "base7b_factored"])
-@pytest.mark.parametrize("T", [1, 16])
+@pytest.mark.parametrize("T", [1, 16, 32])
 def test_table1_factored(preset, T):
     """The Qwen3-235B-A22B and Baseline-7B rows of Table 1 (FACTORED form,
-    group-limited top-k, softmax)."""
+    group-limited top-k, softmax); at 32 tokens units with two token groups
+    and down stages split over two waves."""
     case = Case(P[preset].layer, T, seed=110 + T)
     check_case(case, tokens=sample_tokens(T, 2))
 
