@@ -184,6 +184,11 @@ int token_groups_max(const deamoe_config &c, int T) {
   return (T + gt - 1) / gt;
 }
 
+// Waves sharing one SLICE gate/up tile: four, and two above 32 tokens, where
+// two token tiles leave two waves per SIMD and twice the tiles in flight per
+// workgroup stream faster.
+int slice_gate_up_ks_of(int T) { return T > DEAMOE_SGU_KS4_MAX_T ? 2 : 4; }
+
 // Rows of a down-projection tile: row pairs while the token tiles are few
 // enough for both halves' accumulators to stay in registers.
 int down_rows_of(int) { return DEAMOE_DOWN_PAIR ? 2 * kTile : kTile; }
@@ -414,7 +419,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     const int ta = tiles_bound(act_depts, c.d_shared) +
                    (c.d_private ? tiles_bound(act_exps, c.d_private) : 0) +
                    se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, 4, ta * groups, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, slice_gate_up_ks_of(T),
+                                   ta * groups, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     if (use_chain(c, T)) {   // down projections and combine in one kernel
       ChainArgs ch;

@@ -31,6 +31,11 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #ifndef DEAMOE_SDOWN_KS2_T
 #define DEAMOE_SDOWN_KS2_T 2
 #endif
+// SLICE gate/up stages split K over 4 waves up to this many tokens, over 2
+// above.
+#ifndef DEAMOE_SGU_KS4_MAX_T
+#define DEAMOE_SGU_KS4_MAX_T 32
+#endif
 // K split of the FACTORED department gate/up stage (W_g x, W_u x).
 #ifndef DEAMOE_KS_FGU
 #define DEAMOE_KS_FGU 4

@@ -171,8 +171,10 @@ def test_dsv3_skew_gumbel():
     check_case(case, tokens=sample_tokens(96))
 
 
-@pytest.mark.parametrize("T", [1, 16, 32])
+@pytest.mark.parametrize("T", [1, 16, 32, 64])
 def test_dsv3_fp8(T):
+    """64 tokens: the gate/up stage with two token tiles and a two-wave K
+    split, the separate down stage and the combine."""
     case = Case(P["dsv3_fp8"].layer, T, seed=70 + T)
     check_case(case, tokens=sample_tokens(T))
 
