@@ -92,7 +92,31 @@ def compare_outputs(y_gpu: torch.Tensor, y_ref: np.ndarray, dtype: str, rows=Non
     return err / max(scale, 1e-30)
 
 
-def sample_tokens(T: int, count: int = 3) -> list:
-    if T <= count:
-        return list(range(T))
-    return sorted({0, T // 2, T - 1, *range(min(count - 3, 0))})
+class WeightCache:
+    """One weight draw of a full-size layer shared by the batches that test it
+    (device tensors and their host copies).  Holds one draw at a time, so the
+    device and host memory of a preset is released when the next one is
+    drawn, and all of it by clear()."""
+
+    def __init__(self):
+        self.key, self.w, self.hw = None, None, None
+
+    def get(self, cfg, seed: int, gate_exact: bool = True, host: bool = True):
+        key = (cfg, seed, gate_exact)
+        if key != self.key:
+            self.clear()
+            self.w = W.make_weights(cfg, seed, device="cuda", gate_exact=gate_exact)
+            self.key = key
+        if host and self.hw is None:
+            self.hw = {k: v.cpu() for k, v in self.w.items()}
+        return self.w, self.hw
+
+    def case(self, cfg, T, seed, weight_seed, gate_exact=True, **kw) -> "Case":
+        w, hw = self.get(cfg, weight_seed, gate_exact)
+        c = Case(cfg, T, seed=seed, gate_exact=gate_exact, weights=w, **kw)
+        c._host = hw
+        return c
+
+    def clear(self):
+        self.key, self.w, self.hw = None, None, None
+        torch.cuda.empty_cache()
