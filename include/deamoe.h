@@ -176,6 +176,25 @@ int deamoe_layer_forward(const deamoe_config *cfg, int32_t T, const void *x,
                          const float *router_bias, deamoe_routing *routing_out, void *y,
                          void *ws, size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * call as deamoe_layer_forward, same kernels and results, with the workspace
+ * taken from a library-owned device array of DEAMOE_SCRATCH_BYTES per GPU
+ * (the current device's), held until the process ends.  Nothing is allocated
+ * or freed.  A configuration whose workspace (deamoe_workspace_bytes, sized
+ * for cfg->max_tokens) exceeds DEAMOE_SCRATCH_BYTES returns
+ * DEAMOE_ERR_WORKSPACE before any HIP call.  The first call on a device
+ * resolves that device's array address (DEAMOE_ERR_HIP if that fails).
+ * Every call on one GPU shares its array: calls that overlap in time on one
+ * GPU (other streams, other host threads) race and must be serialised by the
+ * caller.  No part of the array needs clearing between calls; each call
+ * writes everything it reads.  `stream` must belong to the current device. */
+#define DEAMOE_SCRATCH_BYTES (64u << 20)
+int deamoe_layer_forward_noalloc(const deamoe_config *cfg, int32_t T, const void *x,
+                                 const deamoe_weights *w, const float *logits_in,
+                                 const float *router_bias, deamoe_routing *routing_out, void *y,
+                                 void *stream);
+
 /* The same with caller-created hipEvent_t handles recorded on `stream` at the
  * stage boundaries, for timing: events[0] before the router, then one after
  * each launched kernel in order (SLICE: router GEMV, route, gate/up, down,

@@ -3,6 +3,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "gemm_tile.h"
 #include "launch.h"
@@ -513,6 +514,34 @@ int64_t matrix_bytes(int w_dtype, int64_t R, int64_t C) {
   return b;
 }
 
+// Workspace of deamoe_layer_forward_noalloc: one library-owned device array
+// per GPU, held until the process ends.  Host code never passes the array's
+// name to a kernel or a copy: each device's address comes from
+// hipGetSymbolAddress, resolved once per device with that device current.
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kScratchDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[DEAMOE_SCRATCH_BYTES];
+
+namespace {
+
+int scratch_of_current_device(void **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return DEAMOE_ERR_HIP;
+  if (dev < 0 || dev >= kScratchDevices) return DEAMOE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DEAMOE_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DEAMOE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -563,6 +592,24 @@ int deamoe_layer_forward(const deamoe_config *cfg, int32_t T, const void *x,
                          size_t ws_bytes, void *stream) {
   return layer_impl(cfg, T, x, w, logits_in, router_bias, routing_out, y, ws, ws_bytes, stream,
                     nullptr, 0);
+}
+
+int deamoe_layer_forward_noalloc(const deamoe_config *cfg, int32_t T, const void *x,
+                                 const deamoe_weights *w, const float *logits_in,
+                                 const float *router_bias, deamoe_routing *routing_out, void *y,
+                                 void *stream) {
+  // the same validation as the workspace call, and the size limit, before any
+  // HIP call
+  int rc = validate_config(cfg);
+  if (rc) return rc;
+  if (make_layout(*cfg).total > (size_t)DEAMOE_SCRATCH_BYTES) return DEAMOE_ERR_WORKSPACE;
+  if (T < 0) return DEAMOE_ERR_INVALID;
+  if (T > cfg->max_tokens) return DEAMOE_ERR_UNSUPPORTED;
+  if (T == 0) return DEAMOE_OK;   // empty batch: no HIP call
+  void *ws = nullptr;
+  if ((rc = scratch_of_current_device(&ws))) return rc;
+  return layer_impl(cfg, T, x, w, logits_in, router_bias, routing_out, y, ws,
+                    DEAMOE_SCRATCH_BYTES, stream, nullptr, 0);
 }
 
 int deamoe_layer_forward_traced(const deamoe_config *cfg, int32_t T, const void *x,

@@ -22,10 +22,11 @@ FORM_SLICE, FORM_FACTORED = 0, 1
 SCORE_SOFTMAX, SCORE_SIGMOID = 0, 1
 SIGMA_SILU, SIGMA_NONE, SIGMA_GELU, SIGMA_RMSNORM = 0, 1, 2, 3
 MAX_TOKENS = 128
+SCRATCH_BYTES = 64 << 20   # library-owned workspace of deamoe_layer_forward_noalloc, per GPU
 
 EXPORTS = ("deamoe_status_string", "deamoe_workspace_bytes", "deamoe_route",
            "deamoe_layer_forward", "deamoe_layer_forward_traced", "deamoe_baseline_forward",
-           "deamoe_loaded_bytes", "deamoe_trace_points")
+           "deamoe_loaded_bytes", "deamoe_trace_points", "deamoe_layer_forward_noalloc")
 
 
 class DeamoeError(RuntimeError):
@@ -78,6 +79,8 @@ def lib():
         L.deamoe_layer_forward.argtypes = layer_args
         L.deamoe_baseline_forward.argtypes = layer_args
         L.deamoe_layer_forward_traced.argtypes = layer_args + [C.POINTER(C.c_void_p), i32]
+        L.deamoe_layer_forward_noalloc.argtypes = [cfgp, i32, vp, C.POINTER(deamoe_weights), vp, vp,
+                                                   C.POINTER(deamoe_routing), vp, vp]
         L.deamoe_trace_points.argtypes = [cfgp, i32, C.POINTER(C.c_int32)]
         L.deamoe_loaded_bytes.argtypes = [cfgp, i32, vp, vp, C.POINTER(C.c_int64),
                                           C.POINTER(C.c_int64)]
@@ -204,6 +207,16 @@ def deamoe_layer_forward_traced(c: deamoe_config, x, W: deamoe_weights, y, ws, e
     arr = (C.c_void_p * len(events))(*events)
     _layer(lib().deamoe_layer_forward_traced, c, x, W, y, ws, logits_in, router_bias, routing,
            stream, arr, len(events))
+
+
+def deamoe_layer_forward_noalloc(c: deamoe_config, x, W: deamoe_weights, y, logits_in=None,
+                                 router_bias=None, routing: Routing | None = None, stream=None):
+    """deamoe_layer_forward on the library's own per-GPU scratch array (no workspace)."""
+    r = routing.struct() if routing is not None else None
+    _check(lib().deamoe_layer_forward_noalloc(
+        C.byref(c), int(x.shape[0]), _ptr(x), C.byref(W), _ptr(logits_in), _ptr(router_bias),
+        C.byref(r) if r is not None else None, _ptr(y), _stream(stream)),
+        "deamoe_layer_forward_noalloc")
 
 
 def deamoe_baseline_forward(c: deamoe_config, x, W: deamoe_weights, y, ws, logits_in=None,

@@ -156,6 +156,28 @@ def test_layer_validation_paths():
     assert call_layer(c, Wt=Wt, routing=r) == D.ERR_INVALID
 
 
+def test_noalloc_validation_before_any_hip_call():
+    """deamoe_layer_forward_noalloc rejects a configuration whose workspace
+    exceeds the library's scratch array, and returns for T == 0, before any
+    HIP call (so these run without a GPU)."""
+    L = D.lib()
+    cfg = W.PRESETS["dsv3_bf16"].layer
+
+    def call(c, T):
+        return L.deamoe_layer_forward_noalloc(C.byref(c), T, FAKE, None, None, None, None, FAKE,
+                                              None)
+    big = D.make_config(cfg.replace(hidden=14336), 128)
+    assert D.workspace_bytes(big) > D.SCRATCH_BYTES
+    assert call(big, 1) == D.ERR_WORKSPACE
+    assert call(big, 0) == D.ERR_WORKSPACE
+    ok = D.make_config(cfg, 128)
+    assert D.workspace_bytes(ok) <= D.SCRATCH_BYTES
+    assert call(ok, 0) == D.OK
+    assert call(ok, -1) == D.ERR_INVALID
+    assert call(ok, 129) == D.ERR_UNSUPPORTED
+    assert call(D.make_config(cfg.replace(n_depts=7), 16), 1) == D.ERR_INVALID
+
+
 def test_fp8_needs_scales():
     cfg = W.PRESETS["dsv3_fp8"].layer
     c = D.make_config(cfg, 4)
