@@ -224,10 +224,14 @@ int deamoe_baseline_forward(const deamoe_config *cfg, int32_t T, const void *x,
                             const float *router_bias, deamoe_routing *routing_out, void *y,
                             void *ws, size_t ws_bytes, void *stream);
 
-/* Host.  Algorithmic HBM bytes of one step given the realised routing counts
- * (host arrays dept_count [m], exp_count [n]): every touched department's and
- * expert's matrices once (fp8: plus block scales), the router, the shared
- * expert; *total_bytes adds x read and y written (T x h activations each). */
+/* Host.  Algorithmic HBM bytes of one step: the per-step weight loading that
+ * Sec. 3.3 compares between DeaMoE and vanilla MoE (Fig. 2), with the router
+ * counted as that comparison's budget accounting counts it.  Given the
+ * realised routing counts (host arrays dept_count [m], exp_count [n]):
+ * every touched department's and expert's matrices once (fp8: plus block
+ * scales), the router, the shared expert -> *weight_bytes; *total_bytes adds
+ * x read and y written (T x h activations each).  Either output may be NULL.
+ * DEAMOE_ERR_INVALID for a NULL count array or T < 0. */
 int deamoe_loaded_bytes(const deamoe_config *cfg, int32_t T, const int32_t *dept_count,
                         const int32_t *exp_count, int64_t *weight_bytes, int64_t *total_bytes);
 
