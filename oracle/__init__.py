@@ -62,11 +62,14 @@ def _open(path: str):
 
 
 def lib():
+    """The oracle library: oracle/liboracle.so, or the build named by
+    DEAMOE_ORACLE_LIB (the sanitizer build of the CPU tests)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_build.LIB):
+        path = os.environ.get("DEAMOE_ORACLE_LIB", _build.LIB)
+        if path == _build.LIB and not os.path.exists(path):
             _build.build()
-        _lib = _open(_build.LIB)
+        _lib = _open(path)
     return _lib
 
 

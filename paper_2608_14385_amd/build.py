@@ -58,5 +58,42 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host-side sanitizer flags for the C-ABI translation unit (device code is
+# built as usual): AddressSanitizer and UndefinedBehaviorSanitizer, aborting
+# on the first finding.
+SAN_HOST_FLAGS = ("-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined "
+                  "-Xarch_host -fno-sanitize-recover=undefined "
+                  "-Xarch_host -fno-omit-frame-pointer").split()
+
+
+def build_host_sanitized(out_dir: str, verbose: bool = False) -> str:
+    """libdeamoe.so in out_dir with the host code of api.hip (validation,
+    workspace layout, launch sequence) built under ASan and UBSan, linked
+    with the regular objects of the kernel sources.  A process loading it
+    needs clang's ASan runtime preloaded (asan_runtime())."""
+    kernel_objs = [os.path.join(BUILD, s.replace(".hip", ".o")) for s in SOURCES if s != "api.hip"]
+    if not all(os.path.exists(o) for o in kernel_objs):
+        build(verbose)
+    os.makedirs(out_dir, exist_ok=True)
+    obj = os.path.join(out_dir, "api_san.o")
+    cmd = [_hipcc(), *HIPCC_FLAGS, *SAN_HOST_FLAGS, "-g", "-c", os.path.join(CSRC, "api.hip"),
+           "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode:
+        raise RuntimeError("hipcc failed on api.hip (sanitized):\n" + r.stdout + r.stderr)
+    objs = [obj] + kernel_objs
+    lib = os.path.join(out_dir, "libdeamoe.so")
+    cmd = [_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *SAN_HOST_FLAGS[:4],
+           "-shared-libasan", "-o", lib, *objs]
+    subprocess.run(cmd, check=True, capture_output=not verbose)
+    return lib
+
+
+def asan_runtime() -> str:
+    """Path of clang's shared AddressSanitizer runtime (for LD_PRELOAD)."""
+    return subprocess.run([_hipcc(), "-print-file-name=libclang_rt.asan-x86_64.so"], check=True,
+                          capture_output=True, text=True).stdout.strip()
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
