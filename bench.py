@@ -337,6 +337,8 @@ def multi_layer(cfg, base_cfg, L: int, T: int, reps: int) -> dict:
 
 def stage_names(form: str, n_stages: int) -> list:
     if form == "slice":
+        if n_stages == 3:   # routing inside the gate/up launch, fused down and combine
+            return ["router_gemv", "route_gate_up", "down_combine"]
         if n_stages == 4:   # down projections and combine in one kernel
             return ["router_gemv", "route_plan", "gate_up", "down_combine"]
         return ["router_gemv", "route_plan", "gate_up", "down", "combine"]
@@ -525,7 +527,8 @@ def main():
         names = stage_names(cfg.form, len(stages[0]))
         mean = np.mean(np.asarray(stages), axis=0)
         result["kernels_us"] = {n: round(float(v) * 1e3, 2) for n, v in zip(names, mean)}
-        dom = names.index("gate_up" if cfg.form == "slice" else "dept_gate_up")
+        dom = names.index("dept_gate_up" if cfg.form != "slice" else
+                          "route_gate_up" if "route_gate_up" in names else "gate_up")
         gu = [gate_up_bytes(cfg, T, b[2], b[3]) for b in run.bytes]
         gu_bytes = float(np.mean([gu[i % len(gu)] for i in range(args.steps)]))
         achieved = gu_bytes / (mean[dom] * 1e-3) / 1e9

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdeamoe.so")
-SOURCES = ("api.hip", "route.hip", "gemm.hip", "combine.hip", "chain.hip")
+SOURCES = ("api.hip", "route.hip", "gemm.hip", "combine.hip", "chain.hip", "small.hip")
 PROBE_SRC = os.path.join(CSRC, "probe", "read_probe.hip")
 PROBE_LIB = os.path.join(HERE, "libdeamoe_probe.so")
 

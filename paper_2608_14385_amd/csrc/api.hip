@@ -235,6 +235,19 @@ bool use_chain(const deamoe_config &c, int T) {
   return units <= kMaxChainUnits;
 }
 
+// SLICE batches of at most kSmallMaxT tokens route inside the gate/up launch
+// (every workgroup routes the tokens itself; workgroup 0 writes the routing
+// and the fused down kernel's units): one dependent launch fewer, and no
+// unit-table round trip before the weights stream.  Routers of up to 512
+// experts (8 logits per lane).
+#ifndef DEAMOE_SMALL
+#define DEAMOE_SMALL 1
+#endif
+bool use_small(const deamoe_config &c, int T) {
+  return DEAMOE_SMALL && c.form == DEAMOE_FORM_SLICE && T <= kSmallMaxT && use_chain(c, T) &&
+         route_ns(c.n_experts) <= 8;
+}
+
 template <class P>
 P *at(void *ws, size_t off) {
   return reinterpret_cast<P *>(static_cast<char *>(ws) + off);
@@ -258,28 +271,29 @@ int check(hipError_t e) { return e == hipSuccess ? DEAMOE_OK : DEAMOE_ERR_HIP; }
     if (_rc != DEAMOE_OK) return _rc;       \
   } while (0)
 
-// Router product and route/plan kernels.
-int enqueue_route(const deamoe_config &c, int T, const void *x, const void *router_w,
-                  const float *logits_in, const float *bias, const deamoe_routing &r, void *ws,
-                  const Layout &L, int plan, const deamoe_weights *w, Events &ev,
-                  hipStream_t s) {
+// Router product: partial logits over the hidden-dimension chunks.
+int enqueue_router(const deamoe_config &c, int T, const void *x, const void *router_w, void *ws,
+                   const Layout &L, Events &ev, hipStream_t s) {
+  RouterArgs ra;
+  ra.w = router_w;
+  ra.x = x;
+  ra.part = at<float>(ws, L.part);
+  ra.n = c.n_experts;
+  ra.h = c.hidden;
+  ra.T = T;
+  ra.kchunk = c.hidden / L.kc;
+  ra.tiles = (c.n_experts + kTile - 1) / kTile;
+  ra.ldp = 64 * route_ns(c.n_experts);
+  DEAMOE_TRY(launch_router(ra, c.act_dtype == DEAMOE_F32 ? WT_F32 : WT_BF16, ntt_of(T), L.kc, s));
   DEAMOE_TRY(ev.mark());
-  RouteArgs a;
+  return DEAMOE_OK;
+}
+
+// Argument block of the routing kernels (and of the plan they write).
+void fill_route_args(RouteArgs &a, const deamoe_config &c, int T, const void *x,
+                     const float *logits_in, const float *bias, const deamoe_routing &r,
+                     void *ws, const Layout &L, int plan, const deamoe_weights *w) {
   memset(&a, 0, sizeof a);
-  if (!logits_in) {
-    RouterArgs ra;
-    ra.w = router_w;
-    ra.x = x;
-    ra.part = at<float>(ws, L.part);
-    ra.n = c.n_experts;
-    ra.h = c.hidden;
-    ra.T = T;
-    ra.kchunk = c.hidden / L.kc;
-    ra.tiles = (c.n_experts + kTile - 1) / kTile;
-    ra.ldp = 64 * route_ns(c.n_experts);
-    DEAMOE_TRY(launch_router(ra, c.act_dtype == DEAMOE_F32 ? WT_F32 : WT_BF16, ntt_of(T), L.kc, s));
-    DEAMOE_TRY(ev.mark());
-  }
   a.T = T;
   a.n = c.n_experts;
   a.m = c.n_depts;
@@ -332,6 +346,20 @@ int enqueue_route(const deamoe_config &c, int T, const void *x, const void *rout
     a.cunits = at<ChainUnit>(ws, L.cunits);
     a.wdense = at<float>(ws, L.wdense);
   }
+}
+
+// Router product and route/plan kernels.
+int enqueue_route(const deamoe_config &c, int T, const void *x, const void *router_w,
+                  const float *logits_in, const float *bias, const deamoe_routing &r, void *ws,
+                  const Layout &L, int plan, const deamoe_weights *w, Events &ev,
+                  hipStream_t s) {
+  DEAMOE_TRY(ev.mark());
+  if (!logits_in) {
+    const int rc = enqueue_router(c, T, x, router_w, ws, L, ev, s);
+    if (rc) return rc;
+  }
+  RouteArgs a;
+  fill_route_args(a, c, T, x, logits_in, bias, r, ws, L, plan, w);
   DEAMOE_TRY(launch_route(a, s));
   DEAMOE_TRY(ev.mark());
   return DEAMOE_OK;
@@ -399,10 +427,33 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
   Events ev{events, n_events, 0, s};
   const deamoe_routing r = routing_in_ws(ws, L, routing_out);
   const bool slice = c.form == DEAMOE_FORM_SLICE;
+  const int wt = c.w_dtype == DEAMOE_F32 ? WT_F32 : c.w_dtype == DEAMOE_BF16 ? WT_BF16 : WT_FP8;
+  if (use_small(c, T)) {   // router, then routing + gate/up, then the fused down kernel
+    DEAMOE_TRY(ev.mark());
+    if (!logits_in && (rc = enqueue_router(c, T, x, w->router, ws, L, ev, s))) return rc;
+    RouteArgs a;
+    fill_route_args(a, c, T, x, logits_in, bias, r, ws, L, PLAN_SLICE, w);
+    const int dk = L.max_dept_pairs / c.max_tokens;
+    const int items = tiles_bound(std::min(c.n_depts, T * dk), c.d_shared) +
+                      (c.d_private ? tiles_bound(std::min(c.n_experts, T * c.top_k), c.d_private)
+                                   : 0) +
+                      (c.d_shared_expert ? tiles_bound(1, c.d_shared_expert) : 0);
+    DEAMOE_TRY(launch_small_route_gate_up(a, wt, items, s));
+    DEAMOE_TRY(ev.mark());
+    ChainArgs ch;
+    ch.units = at<ChainUnit>(ws, L.cunits);
+    ch.counts = at<PlanCounts>(ws, L.counts)->stage[1];
+    ch.y = y;
+    ch.T = T;
+    ch.h = c.hidden;
+    ch.act_f32 = c.act_dtype == DEAMOE_F32;
+    DEAMOE_TRY(launch_chain(ch, wt, s));
+    DEAMOE_TRY(ev.mark());
+    return DEAMOE_OK;
+  }
   rc = enqueue_route(c, T, x, w->router, logits_in, bias, r, ws, L,
                      slice ? PLAN_SLICE : PLAN_FACTORED, w, ev, s);
   if (rc) return rc;
-  const int wt = c.w_dtype == DEAMOE_F32 ? WT_F32 : c.w_dtype == DEAMOE_BF16 ? WT_BF16 : WT_FP8;
   const int ntt = wave_ntt_of(c, T), groups = token_groups_max(c, T);
   const PlanCounts *pc = at<PlanCounts>(ws, L.counts);
   auto stage = [&](int i) {
@@ -625,7 +676,8 @@ int deamoe_trace_points(const deamoe_config *cfg, int32_t T, int32_t *n_events) 
   const int rc = validate_config(cfg);
   if (rc) return rc;
   if (!n_events || T < 1 || T > cfg->max_tokens) return DEAMOE_ERR_INVALID;
-  *n_events = (cfg->form == DEAMOE_FORM_SLICE ? 6 : 9) - (use_chain(*cfg, T) ? 1 : 0);
+  *n_events = (cfg->form == DEAMOE_FORM_SLICE ? 6 : 9) - (use_chain(*cfg, T) ? 1 : 0) -
+              (use_small(*cfg, T) ? 1 : 0);
   return DEAMOE_OK;
 }
 

@@ -120,6 +120,11 @@ enum GemmMode : int {
 hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int mode, int ntt,
                                int ks, int max_tiles, int grid_cap, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
+// SLICE batches of 1..4 tokens with the fused down kernel (a.chain): routing,
+// the gate/up stage and the down kernel's units in one launch (items: the
+// most 16-row gate/up tiles a step can have).
+hipError_t launch_small_route_gate_up(const RouteArgs &a, int wtype, int items, hipStream_t s);
+constexpr int kSmallMaxT = 4;
 hipError_t launch_chain(const ChainArgs &a, int wtype, hipStream_t s);
 hipError_t launch_zsum(const ZsumArgs &a, int max_dept_pairs, hipStream_t s);
 

@@ -15,8 +15,7 @@
 //   combine slots of every token, and the counts.
 // route_plan_kernel: both of the above in one workgroup for batches of up
 //   to four tokens, the per-token results passed on through LDS.
-#include "gemm_tile.h"
-#include "launch.h"
+#include "route_dev.h"
 
 namespace deamoe {
 
@@ -59,582 +58,6 @@ static hipError_t router_ntt(const RouterArgs &a, int ntt, int kc, hipStream_t s
 
 hipError_t launch_router(const RouterArgs &a, int wtype, int ntt, int kc, hipStream_t s) {
   return wtype == WT_F32 ? router_ntt<WT_F32>(a, ntt, kc, s) : router_ntt<WT_BF16>(a, ntt, kc, s);
-}
-
-// ------------------------------------------------------------ route and plan
-
-__device__ inline bool ranks_before(float va, int a, float vb, int b) {
-  return va > vb || (va == vb && a < b);
-}
-
-// Order-preserving map of a float onto an unsigned int (larger float, larger
-// key).  -0 takes the key of +0: the two are equal values, so a tie between
-// them goes to the lower expert id like any other tie.
-__device__ inline uint32_t ord_u32(float f) {
-  uint32_t u = __float_as_uint(f);
-  u = u == 0x80000000u ? 0u : u;
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-// Wave-wide maximum of a 64-bit key, returned to every lane: DPP exchanges
-// within each row of 16 lanes (xor 1, xor 2, half-row mirror, row mirror),
-// then the four row maxima through readlane.
-__device__ inline uint64_t wave_max_u64(uint64_t v) {
-#define DEAMOE_DPP_STEP(ctrl)                                                               \
-  do {                                                                                      \
-    const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);                              \
-    const uint32_t olo = __builtin_amdgcn_update_dpp(lo, lo, ctrl, 0xf, 0xf, false);        \
-    const uint32_t ohi = __builtin_amdgcn_update_dpp(hi, hi, ctrl, 0xf, 0xf, false);        \
-    const uint64_t o = ((uint64_t)ohi << 32) | olo;                                         \
-    v = o > v ? o : v;                                                                      \
-  } while (0)
-  DEAMOE_DPP_STEP(0xB1);    // quad_perm [1,0,3,2]
-  DEAMOE_DPP_STEP(0x4E);    // quad_perm [2,3,0,1]
-  DEAMOE_DPP_STEP(0x141);   // row_half_mirror
-  DEAMOE_DPP_STEP(0x140);   // row_mirror
-#undef DEAMOE_DPP_STEP
-  uint64_t best = 0;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, 16 * r);
-    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), 16 * r);
-    const uint64_t o = ((uint64_t)hi << 32) | lo;
-    best = o > best ? o : best;
-  }
-  return best;
-}
-
-// Arg-max by (value desc, index asc) over the lanes' candidates; a lane with
-// no candidate passes valid = false.  Returns the winning index (every lane).
-__device__ inline int wave_argmax_idx(float v, int i, bool valid, float &best_v) {
-  const uint64_t key = valid ? (((uint64_t)ord_u32(v) << 32) | (uint32_t)~(uint32_t)i) : 0ull;
-  const uint64_t b = wave_max_u64(key);
-  const uint32_t ob = (uint32_t)(b >> 32);
-  best_v = __uint_as_float((ob & 0x80000000u) ? (ob & 0x7fffffffu) : ~ob);
-  return (int)~(uint32_t)b;
-}
-
-// DPP exchange of a 32-bit value within rows of 16 lanes.
-template <int CTRL>
-__device__ inline float dpp_f32(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL,
-                                                    0xf, 0xf, false));
-}
-
-// Wave-wide sum / maximum returned to every lane: butterflies within each row
-// of 16 lanes (xor 1, xor 2, half-row mirror, row mirror), then the four row
-// results through readlane, combined in row order.
-__device__ inline float wave_sum(float v) {
-  v += dpp_f32<0xB1>(v);
-  v += dpp_f32<0x4E>(v);
-  v += dpp_f32<0x141>(v);
-  v += dpp_f32<0x140>(v);
-  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-  return ((r0 + r1) + r2) + r3;
-}
-
-__device__ inline float wave_max(float v) {
-  v = fmaxf(v, dpp_f32<0xB1>(v));
-  v = fmaxf(v, dpp_f32<0x4E>(v));
-  v = fmaxf(v, dpp_f32<0x141>(v));
-  v = fmaxf(v, dpp_f32<0x140>(v));
-  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
-}
-
-// Inclusive prefix sum over the wave: shifts by 1, 2, 4, 8 within each row
-// of 16 lanes (lanes shifted in from outside the row add 0), then the row
-// totals below each lane's row through readlane.
-__device__ inline int wave_incl_scan(int v) {
-  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
-  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
-  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
-  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
-  const int lane = __lane_id();
-  const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31);
-  const int r2 = __builtin_amdgcn_readlane(v, 47);
-  return v + (lane >= 16 ? r0 : 0) + (lane >= 32 ? r1 : 0) + (lane >= 48 ? r2 : 0);
-}
-
-// Order-preserving float <-> int map for integer max.
-__device__ inline int ord_key(float f) {
-  const int i = __float_as_int(f);
-  return i >= 0 ? i : i ^ 0x7fffffff;
-}
-__device__ inline float ord_val(int i) { return __int_as_float(i >= 0 ? i : i ^ 0x7fffffff); }
-
-// Workgroup barrier that orders LDS accesses only: global stores issued
-// before it may still be in flight.  The route and plan kernels never read
-// back, within a launch, global data they wrote, so their barriers need no
-// more (a full barrier would wait for every outstanding store).
-__device__ inline void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// Exclusive prefix sum of s[0..N) in place, N <= 4 * blockDim; returns the
-// total.  Every thread of the block must call it.
-__device__ int block_exscan(int32_t *s, int N, int32_t *s_tmp) {
-  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
-  const int nwaves = nt / 64;
-  const int per = (N + nt - 1) / nt;
-  const int b = min(tid * per, N), e = min(b + per, N);
-  int local = 0;
-  for (int i = b; i < e; ++i) local += s[i];
-  const int v = wave_incl_scan(local);
-  if (lane == 63) s_tmp[wave] = v;
-  lds_barrier();
-  if (wave == 0) {
-    const int w = wave_incl_scan(lane < nwaves ? s_tmp[lane] : 0);
-    if (lane < nwaves) s_tmp[lane] = w;
-  }
-  lds_barrier();
-  int run = (wave > 0 ? s_tmp[wave - 1] : 0) + v - local;
-  for (int i = b; i < e; ++i) {
-    const int x = s[i];
-    s[i] = run;
-    run += x;
-  }
-  const int total = s_tmp[nwaves - 1];
-  lds_barrier();
-  return total;
-}
-
-// Exclusive prefix sums of two arrays a[0..N) and b[0..N) in place, in one
-// pass (shared barriers); returns both totals.  Every thread of the block
-// must call it; s_tmp holds 2 * (blockDim / 64) values.
-__device__ int2 block_exscan2(int32_t *a, int32_t *b, int N, int32_t *s_tmp) {
-  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
-  const int nwaves = nt / 64;
-  const int per = (N + nt - 1) / nt;
-  const int lo = min(tid * per, N), hi = min(lo + per, N);
-  int la = 0, lb = 0;
-  for (int i = lo; i < hi; ++i) {
-    la += a[i];
-    lb += b[i];
-  }
-  const int va = wave_incl_scan(la), vb = wave_incl_scan(lb);
-  if (lane == 63) {
-    s_tmp[wave] = va;
-    s_tmp[32 + wave] = vb;
-  }
-  lds_barrier();
-  if (wave == 0) {
-    const int wa = wave_incl_scan(lane < nwaves ? s_tmp[lane] : 0);
-    const int wb = wave_incl_scan(lane < nwaves ? s_tmp[32 + lane] : 0);
-    if (lane < nwaves) {
-      s_tmp[lane] = wa;
-      s_tmp[32 + lane] = wb;
-    }
-  }
-  lds_barrier();
-  int ra = (wave > 0 ? s_tmp[wave - 1] : 0) + va - la;
-  int rb = (wave > 0 ? s_tmp[32 + wave - 1] : 0) + vb - lb;
-  for (int i = lo; i < hi; ++i) {
-    const int xa = a[i], xb = b[i];
-    a[i] = ra;
-    b[i] = rb;
-    ra += xa;
-    rb += xb;
-  }
-  const int2 total = make_int2(s_tmp[nwaves - 1], s_tmp[32 + nwaves - 1]);
-  lds_barrier();
-  return total;
-}
-
-__device__ inline void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-constexpr int kMaxKC = 16;   // router chunks (host caps the split)
-
-// Global-address-space view of a pointer.  The plan reads its pointers from
-// an LDS copy of the argument block, which leaves the compiler without the
-// knowledge that they address global memory (stores through them would
-// become flat stores, which also hold up every later LDS wait).
-template <class T>
-using gmem = __attribute__((address_space(1))) T;
-template <class T>
-__device__ inline gmem<T> *glob(T *p) {
-  return reinterpret_cast<gmem<T> *>(reinterpret_cast<uintptr_t>(p));
-}
-
-// Fill one unit of a stage table field by field (no temporary struct).
-__device__ inline void put_unit(gmem<GemmUnit> *U, const void *w0, const void *w1, const float *s0,
-                                const float *s1, const void *in0, const void *in1,
-                                const int32_t *idx, void *out0, void *out1, int R, int K, int ldin,
-                                int ldout, int ntok, int tile_begin, int epi, int out_f32,
-                                int tpg = 1) {
-  U->w0 = w0; U->w1 = w1; U->s0 = s0; U->s1 = s1; U->in0 = in0; U->in1 = in1; U->idx = idx;
-  U->out0 = out0; U->out1 = out1; U->R = R; U->K = K; U->ldw = K; U->ldin = ldin;
-  U->ldout = ldout; U->ntok = ntok; U->tile_begin = tile_begin; U->epi = epi;
-  U->out_f32 = out_f32; U->tpg = tpg;
-}
-
-__device__ inline void put_chain(gmem<ChainUnit> *U, const void *w, const float *s, const void *in,
-                                 const float *pw, int K, uint32_t mask, int step0) {
-  U->w = w; U->s = s; U->in = in; U->pw = pw; U->K = K; U->mask = mask; U->step0 = step0;
-  U->pad_ = 0;
-}
-
-// Row tiles per work item of a stage whose K is not split across waves: short
-// contractions take several tiles so that a work item streams enough bytes.
-__device__ inline int tiles_per_item(int K, int rows, int ks) {
-  return ks > 1 ? 1 : max(1, min(8, 2048 * kTile / (rows * K)));
-}
-__device__ inline int items_of(int R, int tpg, int rows) {
-  return ((R + rows - 1) / rows + tpg - 1) / tpg;
-}
-
-__device__ inline bool bit_at(const uint32_t *row, int i) { return (row[i >> 5] >> (i & 31)) & 1; }
-
-// Number of set bits below bit i of a bitmap row.
-__device__ inline int rank_below(const uint32_t *row, int i) {
-  int r = 0;
-  for (int w = 0; w < (i >> 5); ++w) r += __popc(row[w]);
-  return r + __popc(row[i >> 5] & ((1u << (i & 31)) - 1u));
-}
-
-constexpr int kTW = kMaxT / 32;   // words of a token bitmap
-constexpr int kDW = kMaxM / 32;   // words of a department bitmap
-
-// NS consecutive fp32 values at p (aligned to 4 * NS bytes up to 16).
-template <int NS>
-__device__ inline void load_run(const float *p, float (&v)[NS]) {
-  if constexpr (NS == 1) {
-    v[0] = *p;
-  } else if constexpr (NS == 2) {
-    const float2 q = *reinterpret_cast<const float2 *>(p);
-    v[0] = q.x;
-    v[1] = q.y;
-  } else {
-#pragma unroll
-    for (int i = 0; i < NS / 4; ++i) {
-      const f32x4 q = *reinterpret_cast<const f32x4 *>(p + 4 * i);
-      v[4 * i] = q[0];
-      v[4 * i + 1] = q[1];
-      v[4 * i + 2] = q[2];
-      v[4 * i + 3] = q[3];
-    }
-  }
-}
-
-__device__ inline int popc64(uint64_t v) { return __popcll(v); }
-
-// One wave routes one token: logits, optional group limit, top-k, routing
-// weights and the token's distinct departments with P_{t,j}; the token's
-// combine slots when a plan follows.
-//
-// Top-k works on order keys (a monotone map of the logit to an unsigned
-// int).  A threshold is found by radix selection (built bit by bit from the
-// top; a bit stays if at least k keys reach the value), first over the
-// per-lane maxima; the few candidates at or above it rank themselves by
-// (logit desc, id asc) through LDS.
-struct TokSmem {
-  uint64_t sel[64];                  // candidates in expert order
-  uint64_t ord[kMaxK];               // winners in rank order
-  int32_t gs[kMaxMGrouped];          // department scores (group limit)
-  uint32_t db[kDW];                  // the token's department bitmap
-};
-
-// Per-token results handed to a plan in the same workgroup through LDS
-// (all null when the plan runs as its own kernel).
-struct PlanIn {
-  int32_t *ids, *dep, *nd;
-};
-
-template <int NS>
-__device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSmem &sm,
-                          PlanIn lds = {nullptr, nullptr, nullptr}) {
-  uint64_t *s_sel = sm.sel, *s_ord = sm.ord;
-  int32_t *s_gs = sm.gs;
-  uint32_t *s_db = sm.db;
-  const int n = a.n, k = a.k, E = a.E, m = a.m;
-  const int dwords = (m + 31) / 32;
-  const int e0 = lane * NS;
-  if (lane < dwords) s_db[lane] = 0;
-
-  float lv[NS];
-  {
-    float l[NS];
-    if (a.logits_in) {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) l[s] = a.logits_in[(size_t)t * n + min(e0 + s, n - 1)];
-    } else {
-      // partial sums of the router chunks, added in chunk order; loads of a
-      // batch are issued together (chunks past kc re-read the last one)
-      constexpr int CB = NS >= 4 ? 64 / NS : 16;
-      const float *p = a.part + (size_t)t * a.ldp + e0;
-      const size_t cs = (size_t)a.T * a.ldp;
-      for (int c0 = 0; c0 < a.kc; c0 += CB) {
-        float pc[CB][NS];
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb) load_run<NS>(p + (size_t)min(c0 + cb, a.kc - 1) * cs, pc[cb]);
-        // selects, not branches: a branch here would serialize the loads
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb) {
-          const int c = c0 + cb;
-#pragma unroll
-          for (int s = 0; s < NS; ++s) {
-            const float sum = l[s] + pc[cb][s];
-            l[s] = c == 0 ? pc[cb][s] : (c < a.kc ? sum : l[s]);
-          }
-        }
-      }
-    }
-    if (a.bias) {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) l[s] = l[s] + a.bias[min(e0 + s, n - 1)];
-    }
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      if (e0 + s < n) a.r.logits[(size_t)t * n + e0 + s] = l[s];
-      lv[s] = (e0 + s < n && l[s] == l[s]) ? l[s] : -INFINITY;   // NaN ranks last
-    }
-  }
-
-  // departments of the lane's experts: one division, then stepped along the
-  // run (a division by the runtime E is a long instruction sequence)
-  int dep[NS];
-  {
-    int d = e0 / E, r = e0 - d * E;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      dep[s] = d;
-      const bool wrap = ++r == E;
-      r = wrap ? 0 : r;
-      d = wrap ? d + 1 : d;
-    }
-  }
-
-  // group-limited top-k: keep the kdept departments with the largest maximum
-  // logit (ties to the lower department id)
-  uint64_t keep = ~0ull;
-  if (a.kdept > 0) {
-    if (lane < m) s_gs[lane] = ord_key(-INFINITY);
-    wave_lds_sync();
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-      if (e0 + s < n) atomicMax(&s_gs[dep[s]], ord_key(lv[s]));
-    wave_lds_sync();
-    const float gsv = lane < m ? ord_val(s_gs[lane]) : -INFINITY;
-    keep = 0;
-    for (int r = 0; r < a.kdept; ++r) {
-      float bv;
-      const int bj = wave_argmax_idx(gsv, lane, lane < m && !((keep >> lane) & 1), bv);
-      keep |= 1ull << (bj & 63);
-    }
-  }
-
-  // order keys; experts that may not be chosen get 0, below every eligible
-  // key (the key of -inf is 0x007fffff)
-  uint32_t key[NS];
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    const int e = e0 + s;
-    const bool ok = e < n && (a.kdept == 0 || ((keep >> (dep[s] & 63)) & 1));
-    key[s] = ok ? ord_u32(lv[s]) : 0u;
-  }
-  // Candidates.  theta, the k-th largest of the per-lane maxima, bounds the
-  // k-th largest key from below (k lanes hold a key >= theta), so every
-  // winner has a key >= theta; usually only a few keys reach it.  When more
-  // than 64 do, the exact k-th largest key tau is found by radix selection
-  // and the candidates are exactly the k winners.
-  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
-  uint32_t lmax = 0;
-#pragma unroll
-  for (int s = 0; s < NS; ++s) lmax = max(lmax, key[s]);
-  uint32_t theta = 0;
-  for (int b = 31; b >= 0; --b) {
-    const uint32_t cand = theta | (1u << b);
-    if (popc64(__ballot(lmax >= cand)) >= k) theta = cand;
-  }
-  int ncand = 0;
-#pragma unroll
-  for (int s = 0; s < NS; ++s) ncand += popc64(__ballot(key[s] >= theta));
-  uint32_t selbits = 0;
-  if (ncand <= 64) {
-#pragma unroll
-    for (int s = 0; s < NS; ++s) selbits |= (uint32_t)(key[s] >= theta) << s;
-  } else {
-    uint32_t tau = 0;
-    for (int b = 31; b >= 0; --b) {
-      const uint32_t cand = tau | (1u << b);
-      int cnt = 0;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) cnt += popc64(__ballot(key[s] >= cand));
-      if (cnt >= k) tau = cand;
-    }
-    // keys above tau are fewer than k; the rest come from the keys equal to
-    // tau in ascending expert order (lanes first, then s)
-    int cnt_gt = 0, ties = 0;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      cnt_gt += popc64(__ballot(key[s] > tau));
-      ties += popc64(__ballot(key[s] == tau) & below);
-    }
-    const int need = k - cnt_gt;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const bool eq = key[s] == tau;
-      if (key[s] > tau || (eq && ties < need)) selbits |= 1u << s;
-      ties += eq;
-    }
-    ncand = k;
-  }
-  // candidates to LDS in expert order, then each ranks itself by (key desc,
-  // expert asc); the k best land in rank order
-  int pos = 0;
-#pragma unroll
-  for (int s = 0; s < NS; ++s) pos += popc64(__ballot((selbits >> s) & 1) & below);
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    if ((selbits >> s) & 1) {
-      s_sel[pos] = ((uint64_t)key[s] << 32) | (uint32_t)~(uint32_t)(e0 + s);
-      ++pos;
-    }
-  }
-  wave_lds_sync();
-  if (lane < ncand) {
-    // a batch of 8 LDS reads is issued before any is compared (entries past
-    // ncand are read but not counted)
-    const uint64_t mine = s_sel[lane];
-    int rank = 0;
-    for (int j0 = 0; j0 < ncand; j0 += 8) {
-      uint64_t v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = s_sel[(j0 + u) & 63];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) rank += (j0 + u < ncand) & (v[u] > mine);
-    }
-    if (rank < k) s_ord[rank] = mine;
-  }
-  wave_lds_sync();
-  const bool sel = lane < k;
-  uint64_t kk = sel ? s_ord[lane] : 0ull;
-  // Strict coverage (Sec. 3.4).  While the k winners span fewer than kdept
-  // departments, the lowest-ranked winner whose department holds another
-  // winner gives way to the best eligible expert (key != 0: a kept
-  // department) of a department not yet covered, and the winners are ranked
-  // again.  Each round covers one more department.
-  if (a.dept_cover) {
-    for (int it = 0; it < a.kdept; ++it) {
-      const int dl = sel ? (int)(~(uint32_t)kk) / E : 0;
-      uint64_t cov = 0;
-      int mult = 0;
-      for (int q = 0; q < k; ++q) {
-        const int dq = __builtin_amdgcn_readlane(dl, q);
-        cov |= 1ull << (dq & 63);
-        mult += dq == dl;
-      }
-      if (popc64(cov) >= a.kdept) break;
-      uint64_t best = 0;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const int e = e0 + s;
-        const uint64_t c = ((uint64_t)key[s] << 32) | (uint32_t)~(uint32_t)e;
-        if (key[s] != 0u && !((cov >> (dep[s] & 63)) & 1) && c > best) best = c;
-      }
-      best = wave_max_u64(best);
-      const uint64_t vm = __ballot(sel && mult >= 2);
-      if (vm == 0 || best == 0) break;   // not reached when k >= kdept
-      if (lane == 63 - __clzll(vm)) kk = best;
-      if (sel) s_ord[lane] = kk;
-      wave_lds_sync();
-      int rank = 0;
-      for (int j = 0; j < k; ++j) rank += s_ord[j] > kk;
-      wave_lds_sync();
-      if (sel) s_ord[rank] = kk;
-      wave_lds_sync();
-      kk = sel ? s_ord[lane] : 0ull;
-      wave_lds_sync();
-    }
-  }
-  const int my_id = sel ? (int)~(uint32_t)kk : 0;
-  const uint32_t ob = (uint32_t)(kk >> 32);
-  const float my_l = __uint_as_float((ob & 0x80000000u) ? (ob & 0x7fffffffu) : ~ob);
-
-  // routing weights
-  float p;
-  if (a.score == DEAMOE_SCORE_SOFTMAX) {
-    float mx, den;
-    if (a.renorm) {
-      mx = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_l), 0));
-      den = wave_sum(sel ? expf(my_l - mx) : 0.f);
-    } else {
-      float lm = -INFINITY;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) lm = fmaxf(lm, lv[s]);
-      mx = wave_max(lm);
-      float ls = 0.f;
-#pragma unroll
-      for (int s = 0; s < NS; ++s)
-        if (e0 + s < n) ls += expf(lv[s] - mx);
-      den = wave_sum(ls);
-    }
-    p = expf(my_l - mx) / den;
-  } else {
-    const float sg = 1.0f / (1.0f + expf(-my_l));
-    p = a.renorm ? sg / wave_sum(sel ? sg : 0.f) : sg;
-  }
-  p *= a.route_scale;
-  const int d = sel ? my_id / E : 0;
-  if (sel) {
-    a.r.topk_ids[t * k + lane] = my_id;
-    if (lds.ids) lds.ids[t * k + lane] = my_id;
-    a.r.topk_w[t * k + lane] = p;
-    if (a.wdense) glob(a.wdense)[(size_t)(a.m + my_id) * kChainT + t] = p;
-    atomicOr(&s_db[d >> 5], 1u << (d & 31));
-  }
-  wave_lds_sync();
-  // distinct departments, ascending, each with the weights of its selected
-  // experts summed in rank order
-  int nd = 0;
-  for (int w = 0; w < dwords; ++w) nd += __popc(s_db[w]);
-  nd = __builtin_amdgcn_readfirstlane(nd);
-  float P = 0.f;
-  uint32_t eqm = 0;
-  for (int q = 0; q < k; ++q) {
-    const int dq = __builtin_amdgcn_readlane(d, q);
-    const float pq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p), q));
-    if (dq == d) { P += pq; eqm |= 1u << q; }
-  }
-  const bool first = sel && (eqm & ((1u << lane) - 1u)) == 0;
-  const bool slice = a.plan == PLAN_SLICE;
-  const bool exp_slots = slice && a.d_p > 0;
-  const int S = a.max_slots;
-  if (first) {
-    const int dpos = rank_below(s_db, d);
-    a.r.tok_depts[t * k + dpos] = d;
-    if (lds.dep) lds.dep[t * k + dpos] = d;
-    a.r.tok_dept_w[t * k + dpos] = P;
-    if (a.wdense) glob(a.wdense)[(size_t)d * kChainT + t] = P;
-    if (a.plan) a.slot_w[(size_t)t * S + dpos] = slice ? P : 1.0f;
-  }
-  if (lane >= nd && lane < k) {
-    a.r.tok_depts[t * k + lane] = -1;
-    if (lds.dep) lds.dep[t * k + lane] = -1;
-    a.r.tok_dept_w[t * k + lane] = 0.f;
-  }
-  if (a.plan && exp_slots && sel) a.slot_w[(size_t)t * S + nd + lane] = p;
-  if (lane == 0) {
-    a.r.tok_ndept[t] = nd;
-    if (lds.nd) lds.nd[t] = nd;
-    if (a.plan) {
-      const int ns = nd + (exp_slots ? k : 0);
-      if (a.d_se > 0) a.slot_w[(size_t)t * S + ns] = 1.0f;
-      a.nslot[t] = ns + (a.d_se > 0 ? 1 : 0);
-    }
-  }
 }
 
 template <int NS>
@@ -985,18 +408,6 @@ __device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, Pla
   }
 }
 
-// The argument block copied to LDS by the first threads of the workgroup
-// (visible after the next barrier): the plan then loads each pointer where it
-// uses it instead of holding all of them in scalar registers, which spilled.
-template <int BT>
-__device__ inline void args_to_lds(const RouteArgs &a, RouteArgs &sa) {
-  static_assert(sizeof(RouteArgs) % 4 == 0 && sizeof(RouteArgs) / 4 <= BT, "argument copy");
-  const int tid = threadIdx.x;
-  if (tid < (int)(sizeof(RouteArgs) / 4))
-    __builtin_memcpy(reinterpret_cast<char *>(&sa) + 4 * tid,
-                     reinterpret_cast<const char *>(&a) + 4 * tid, 4);
-}
-
 template <int BT>
 __global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
   __shared__ PlanSmem sm;
@@ -1024,7 +435,7 @@ __global__ __launch_bounds__(fused_waves<NS>() * 64) void route_plan_kernel(Rout
   __shared__ RouteArgs sa;
   const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
   args_to_lds<fused_waves<NS>() * 64>(a, sa);
-  if (w < a.T) route_one<NS>(a, w, lane, tsm[w], PlanIn{psm.ids, psm.dep, psm.nd});
+  if (w < a.T) route_one<NS>(a, w, lane, tsm[w], PlanIn{psm.ids, psm.dep, psm.nd, nullptr});
   lds_barrier();
   plan_body<fused_waves<NS>() * 64, true>(sa, psm);
 }

@@ -267,11 +267,15 @@ def test_read_probe_library_exports():
 
 def test_trace_points():
     """Stage boundaries of the traced call: small batches run the last down
-    stage and the combine as one kernel."""
+    stage and the combine as one kernel; SLICE batches of at most 4 tokens
+    also route inside the gate/up launch."""
     c = cfg_c3()
-    assert [D.deamoe_trace_points(c, T) for T in (1, 4, 16, 17, 32, 33, 64)] == [5, 5, 5, 5, 5, 6, 6]
+    assert [D.deamoe_trace_points(c, T) for T in (1, 4, 5, 16, 17, 32, 33, 64)] == \
+        [4, 4, 5, 5, 5, 5, 6, 6]
     s7 = D.make_config(W.PRESETS["7b_bf16"].layer, 64)     # h 2048: fused up to 4 tokens
-    assert [D.deamoe_trace_points(s7, T) for T in (1, 4, 5, 16)] == [5, 5, 6, 6]
+    assert [D.deamoe_trace_points(s7, T) for T in (1, 4, 5, 16)] == [4, 4, 6, 6]
+    # routers of more than 512 experts keep the separate routing kernel
+    assert D.deamoe_trace_points(cfg_c3(n_experts=1024, n_depts=32), 1) == 5
     f = D.make_config(W.PRESETS["dsv3_factored"].layer, 64)
     assert [D.deamoe_trace_points(f, T) for T in (1, 16, 17)] == [8, 8, 9]
     q = D.make_config(W.PRESETS["qwen3_factored"].layer, 64)   # h 4096: separate stages
