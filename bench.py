@@ -335,18 +335,23 @@ def multi_layer(cfg, base_cfg, L: int, T: int, reps: int) -> dict:
     return out
 
 
-def stage_names(form: str, n_stages: int) -> list:
-    if form == "slice":
-        if n_stages == 3:   # routing inside the gate/up launch, fused down and combine
-            return ["router_gemv", "route_gate_up", "down_combine"]
-        if n_stages == 4:   # down projections and combine in one kernel
-            return ["router_gemv", "route_plan", "gate_up", "down_combine"]
-        return ["router_gemv", "route_plan", "gate_up", "down", "combine"]
-    if n_stages == 7:   # department down projections and combine in one kernel
-        return ["router_gemv", "route_plan", "dept_gate_up", "priv_gate_up", "priv_down",
-                "z_collect", "dept_down_combine"]
-    return ["router_gemv", "route_plan", "dept_gate_up", "priv_gate_up", "priv_down", "z_collect",
-            "dept_down", "combine"]
+def routes_in_first_stage(cfg, T: int) -> bool:
+    """Batches of at most 4 tokens with routers of at most 1024 experts route
+    inside the first expert stage's launch (no separate route/plan kernel)."""
+    return T <= 4 and cfg.n_experts <= 1024
+
+
+def stage_names(cfg, T: int, n_stages: int) -> list:
+    """Names of the traced call's stages (between its recorded events)."""
+    small = routes_in_first_stage(cfg, T)
+    if cfg.form == "slice":
+        names = ["router_gemv"] + (["route_gate_up"] if small else ["route_plan", "gate_up"])
+        fused = len(names) + 1 == n_stages   # down projections and combine in one kernel
+        return names + (["down_combine"] if fused else ["down", "combine"])
+    names = ["router_gemv"] + (["route_dept_gate_up"] if small else ["route_plan", "dept_gate_up"])
+    names += ["priv_gate_up", "priv_down", "z_collect"]
+    fused = len(names) + 1 == n_stages
+    return names + (["dept_down_combine"] if fused else ["dept_down", "combine"])
 
 
 def gate_up_bytes(cfg, T: int, dept_count, exp_count) -> int:
@@ -524,11 +529,10 @@ def main():
     # per-kernel durations (HIP events on the launch stream, same region shape)
     if not args.no_stages:
         stages = run.time_stages(hip, args.steps)
-        names = stage_names(cfg.form, len(stages[0]))
+        names = stage_names(cfg, T, len(stages[0]))
         mean = np.mean(np.asarray(stages), axis=0)
         result["kernels_us"] = {n: round(float(v) * 1e3, 2) for n, v in zip(names, mean)}
-        dom = names.index("dept_gate_up" if cfg.form != "slice" else
-                          "route_gate_up" if "route_gate_up" in names else "gate_up")
+        dom = [i for i, n in enumerate(names) if n.endswith("gate_up") and "priv" not in n][0]
         gu = [gate_up_bytes(cfg, T, b[2], b[3]) for b in run.bytes]
         gu_bytes = float(np.mean([gu[i % len(gu)] for i in range(args.steps)]))
         achieved = gu_bytes / (mean[dom] * 1e-3) / 1e9

@@ -184,6 +184,21 @@ int token_groups_max(const deamoe_config &c, int T) {
   const int gt = kTile * wave_ntt_of(c, T);
   return (T + gt - 1) / gt;
 }
+// Token tiles per wave in the separate down stages.  The SLICE down stage
+// keeps one tile up to 64 tokens: its row-pair tiles then fit three waves
+// per SIMD (two with two tiles), which outweighs streaming the rows of a
+// unit with more than 16 tokens once per group (same-process A/B, us per
+// step, two tiles -> one: DeepSeek-V3 shape 764.7 -> 748.3 at 48 tokens,
+// 827.2 -> 824.1 at 64; fp8 505.7 -> 494.5 and the 7B-class layer 119.6 ->
+// 112.9 at 64).  With 128 tokens routing is usually skewed enough that the
+// extra passes cost more (the skewed preset 510.1 -> 520.4).
+int down_ntt_of(const deamoe_config &c, int T) {
+  return c.form == DEAMOE_FORM_SLICE && T <= 64 ? 1 : wave_ntt_of(c, T);
+}
+int down_groups_max(const deamoe_config &c, int T) {
+  const int gt = kTile * down_ntt_of(c, T);
+  return (T + gt - 1) / gt;
+}
 
 // Waves sharing one SLICE gate/up tile: four, and two above 32 tokens, where
 // two token tiles leave two waves per SIMD and twice the tiles in flight per
@@ -235,17 +250,31 @@ bool use_chain(const deamoe_config &c, int T) {
   return units <= kMaxChainUnits;
 }
 
-// SLICE batches of at most kSmallMaxT tokens route inside the gate/up launch
-// (every workgroup routes the tokens itself; workgroup 0 writes the routing
-// and the fused down kernel's units): one dependent launch fewer, and no
-// unit-table round trip before the weights stream.  Routers of up to 512
-// experts (8 logits per lane).
-#ifndef DEAMOE_SMALL
-#define DEAMOE_SMALL 1
-#endif
+// Upper bound of the row tiles of a stage, for the grid size.
+int tiles_bound(int units_max, int R, int rows = kTile) {
+  return units_max * ((R + rows - 1) / rows);
+}
+
+// Tiles of the first expert stage a step of T tokens can have at most.
+int first_stage_items(const deamoe_config &c, int T) {
+  const int dk = std::min(c.top_k_dept > 0 ? c.top_k_dept : c.top_k, std::min(c.top_k, c.n_depts));
+  const bool slice = c.form == DEAMOE_FORM_SLICE;
+  return tiles_bound(std::min(c.n_depts, T * dk), c.d_shared) +
+         (slice && c.d_private ? tiles_bound(std::min(c.n_experts, T * c.top_k), c.d_private)
+                               : 0) +
+         (c.d_shared_expert ? tiles_bound(1, c.d_shared_expert) : 0);
+}
+
+// Batches of at most kSmallMaxT tokens route inside the launch of the first
+// expert stage (every workgroup routes the tokens itself; workgroup 0
+// publishes the routing and runs the plan): one dependent launch fewer, and
+// no unit-table round trip before the weights stream, where that pays off
+// (small_route_pays).
 bool use_small(const deamoe_config &c, int T) {
-  return DEAMOE_SMALL && c.form == DEAMOE_FORM_SLICE && T <= kSmallMaxT && use_chain(c, T) &&
-         route_ns(c.n_experts) <= 8;
+  const int wt = c.w_dtype == DEAMOE_F32 ? WT_F32 : c.w_dtype == DEAMOE_BF16 ? WT_BF16 : WT_FP8;
+  return T <= kSmallMaxT &&
+         small_route_pays(wt, c.n_experts, c.hidden, wbytes_of(c.w_dtype),
+                          c.top_k_dept > 0, first_stage_items(c, T));
 }
 
 template <class P>
@@ -315,6 +344,8 @@ void fill_route_args(RouteArgs &a, const deamoe_config &c, int T, const void *x,
   a.down_rows = down_rows_of(T);
   a.down_ks = down_ks_of(c, T);
   a.wave_tokens = kTile * wave_ntt_of(c, T);
+  a.wave_tokens_b = kTile * down_ntt_of(c, T);
+  a.sigma = c.sigma;
   a.part = at<float>(ws, L.part);
   a.kc = L.kc;
   a.ldp = 64 * route_ns(c.n_experts);
@@ -392,10 +423,6 @@ bool routing_complete(const deamoe_routing &r) {
          r.dept_offset && r.dept_tokens && r.exp_count && r.exp_offset && r.exp_tokens;
 }
 
-// Upper bound of the row tiles of a stage, for the grid size.
-int tiles_bound(int units_max, int R, int rows = kTile) {
-  return units_max * ((R + rows - 1) / rows);
-}
 
 // Launch of a down-projection stage.
 hipError_t launch_down(const GemmStage &st, int wt, int T, int ntt, int groups, int ks,
@@ -428,32 +455,19 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
   const deamoe_routing r = routing_in_ws(ws, L, routing_out);
   const bool slice = c.form == DEAMOE_FORM_SLICE;
   const int wt = c.w_dtype == DEAMOE_F32 ? WT_F32 : c.w_dtype == DEAMOE_BF16 ? WT_BF16 : WT_FP8;
-  if (use_small(c, T)) {   // router, then routing + gate/up, then the fused down kernel
+  const bool small = use_small(c, T);
+  if (small) {   // router, then routing + plan + the first expert stage in one launch
     DEAMOE_TRY(ev.mark());
     if (!logits_in && (rc = enqueue_router(c, T, x, w->router, ws, L, ev, s))) return rc;
     RouteArgs a;
-    fill_route_args(a, c, T, x, logits_in, bias, r, ws, L, PLAN_SLICE, w);
-    const int dk = L.max_dept_pairs / c.max_tokens;
-    const int items = tiles_bound(std::min(c.n_depts, T * dk), c.d_shared) +
-                      (c.d_private ? tiles_bound(std::min(c.n_experts, T * c.top_k), c.d_private)
-                                   : 0) +
-                      (c.d_shared_expert ? tiles_bound(1, c.d_shared_expert) : 0);
-    DEAMOE_TRY(launch_small_route_gate_up(a, wt, items, s));
-    DEAMOE_TRY(ev.mark());
-    ChainArgs ch;
-    ch.units = at<ChainUnit>(ws, L.cunits);
-    ch.counts = at<PlanCounts>(ws, L.counts)->stage[1];
-    ch.y = y;
-    ch.T = T;
-    ch.h = c.hidden;
-    ch.act_f32 = c.act_dtype == DEAMOE_F32;
-    DEAMOE_TRY(launch_chain(ch, wt, s));
-    DEAMOE_TRY(ev.mark());
-    return DEAMOE_OK;
+    fill_route_args(a, c, T, x, logits_in, bias, r, ws, L, slice ? PLAN_SLICE : PLAN_FACTORED,
+                    w);
+    DEAMOE_TRY(launch_small_route_gate_up(a, wt, first_stage_items(c, T), s));
+  } else {
+    rc = enqueue_route(c, T, x, w->router, logits_in, bias, r, ws, L,
+                       slice ? PLAN_SLICE : PLAN_FACTORED, w, ev, s);
+    if (rc) return rc;
   }
-  rc = enqueue_route(c, T, x, w->router, logits_in, bias, r, ws, L,
-                     slice ? PLAN_SLICE : PLAN_FACTORED, w, ev, s);
-  if (rc) return rc;
   const int ntt = wave_ntt_of(c, T), groups = token_groups_max(c, T);
   const PlanCounts *pc = at<PlanCounts>(ws, L.counts);
   auto stage = [&](int i) {
@@ -471,8 +485,9 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
     const int ta = tiles_bound(act_depts, c.d_shared) +
                    (c.d_private ? tiles_bound(act_exps, c.d_private) : 0) +
                    se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, slice_gate_up_ks_of(T),
-                                   ta * groups, kGridCap, s));
+    if (!small)
+      DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, slice_gate_up_ks_of(T),
+                                     ta * groups, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     if (use_chain(c, T)) {   // down projections and combine in one kernel
       ChainArgs ch;
@@ -487,14 +502,15 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
       return DEAMOE_OK;
     }
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
-    DEAMOE_TRY(launch_down(stage(1), wt, T, ntt, groups, down_ks_of(c, T), units, c.hidden,
-                           kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(1), wt, T, down_ntt_of(c, T), down_groups_max(c, T),
+                           down_ks_of(c, T), units, c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
   } else {
     const int d = c.d_shared;
     const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
-    DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, DEAMOE_KS_FGU, t0 * groups,
-                                   kGridCap, s));
+    if (!small)
+      DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, DEAMOE_KS_FGU, t0 * groups,
+                                     kGridCap, s));
     if (c.sigma == DEAMOE_SIGMA_RMSNORM) {   // timed with stage 0
       RowNormArgs na;
       na.counts = pc;

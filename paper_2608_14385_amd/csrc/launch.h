@@ -40,7 +40,9 @@ struct RouteArgs {
   int32_t h, d_s, d_p, d_se, act_f32, w_bytes, fp8, plan;
   int32_t down_rows;     // weight rows of a down-projection tile (16, or 32 for row pairs)
   int32_t down_ks;       // waves sharing one down-projection tile (K split)
-  int32_t wave_tokens;   // tokens of one token group of the expert stages (16 * NTT)
+  int32_t wave_tokens;   // tokens of one token group of the gate/up stages (16 * NTT)
+  int32_t wave_tokens_b; // the same for the down stages
+  int32_t sigma;         // DEAMOE_SIGMA_* of the FACTORED gate/up stage
   // logits: sum of kc partial products, or injected; optional bias
   const float *part;
   int32_t kc, ldp;
@@ -124,6 +126,10 @@ hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 // the gate/up stage and the down kernel's units in one launch (items: the
 // most 16-row gate/up tiles a step can have).
 hipError_t launch_small_route_gate_up(const RouteArgs &a, int wtype, int items, hipStream_t s);
+// Whether that launch pays off: a short routing prologue (no group limit),
+// short tiles (persistent workgroups route once), or every tile resident in
+// one round.  Routers of at most 1024 experts.
+bool small_route_pays(int wtype, int n, int h, int w_bytes, bool group_limited, int items);
 constexpr int kSmallMaxT = 4;
 hipError_t launch_chain(const ChainArgs &a, int wtype, hipStream_t s);
 hipError_t launch_zsum(const ZsumArgs &a, int max_dept_pairs, hipStream_t s);

@@ -235,7 +235,12 @@ __device__ inline void put_chain(gmem<ChainUnit> *U, const void *w, const float 
 // Row tiles per work item of a stage whose K is not split across waves: short
 // contractions take several tiles so that a work item streams enough bytes.
 __device__ inline int tiles_per_item(int K, int rows, int ks) {
-  return ks > 1 ? 1 : max(1, min(8, 2048 * kTile / (rows * K)));
+  if (ks > 1) return 1;
+  int t = max(1, min(8, 2048 * kTile / (rows * K)));
+  // fp8: the item's block scales, (t * rows / 128 + 1) scale rows of K / 128,
+  // fit the 64-entry window of a work item
+  while (t > 1 && (t * rows / 128 + 1) * (K / 128) > 64) --t;
+  return t;
 }
 __device__ inline int items_of(int R, int tpg, int rows) {
   return ((R + rows - 1) / rows + tpg - 1) / tpg;
@@ -373,9 +378,20 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
   if (a.kdept > 0) {
     if (lane < m) s_gs[lane] = ord_key(-INFINITY);
     wave_lds_sync();
+    // the lane's run of experts spans few departments: one atomic per
+    // department of the run, with the run's maximum in it
+    int cur = dep[0], best = ord_key(-INFINITY);
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
-      if (e0 + s < n) atomicMax(&s_gs[dep[s]], ord_key(lv[s]));
+    for (int s = 0; s < NS; ++s) {
+      if (e0 + s >= n) break;
+      if (dep[s] != cur) {
+        atomicMax(&s_gs[cur], best);
+        cur = dep[s];
+        best = ord_key(-INFINITY);
+      }
+      best = max(best, ord_key(lv[s]));
+    }
+    if (e0 < n) atomicMax(&s_gs[cur], best);
     wave_lds_sync();
     const float gsv = lane < m ? ord_val(s_gs[lane]) : -INFINITY;
     keep = 0;
@@ -627,6 +643,379 @@ __device__ inline void args_to_lds(const RouteArgs &a, RouteArgs &sa) {
   if (tid < (int)(sizeof(RouteArgs) / 4))
     __builtin_memcpy(reinterpret_cast<char *>(&sa) + 4 * tid,
                      reinterpret_cast<const char *>(&a) + 4 * tid, 4);
+}
+
+// One workgroup: the per-department and per-expert token lists (ascending
+// token order) from the per-token results, then the unit tables of every
+// expert stage and the combine slots.
+//
+// Membership is kept as token bitmaps in LDS for every expert and
+// department.  A token's position in a CSR list is the offset of the list
+// plus the number of member tokens below it, so every (token, rank) pair is
+// placed independently.  Counts and the number of active units are summed
+// in one scan over departments then experts, packed as count | active << 16
+// (both sums stay below 2^16).
+// MT: the most tokens the plan serves (token bitmaps of MT / 32 words).
+template <int MT>
+struct PlanSmemT {
+  static constexpr int TW = (MT + 31) / 32;
+  static constexpr int MAXT = MT;
+  int32_t ids[MT * kMaxK];           // [t][rank] selected expert
+  int32_t dep[MT * kMaxK];           // [t][slot] departments, -1 padded
+  uint32_t etok[kMaxN * TW];         // [e] token bitmap
+  uint32_t dtok[kMaxM * TW];         // [j] token bitmap
+  int32_t scan[kMaxM + kMaxN];       // [depts, experts] packed prefix
+  int32_t nd[MT];
+  int32_t tmp[64];
+};
+using PlanSmem = PlanSmemT<kMaxT>;
+
+// Every thread of the workgroup (BT threads) calls it.  LDS_IN: the
+// per-token results are already in sm.ids, sm.dep and sm.nd.  PS: a
+// PlanSmemT; with fewer than 32 tokens per bitmap word the unit item
+// prefixes must be closed forms (one token group per unit).
+template <int BT, bool LDS_IN = false, class PS = PlanSmem>
+__device__ __attribute__((always_inline)) void plan_body(const RouteArgs &a, PS &sm) {
+  constexpr int EPT = kMaxN / BT;   // experts per thread in the per-expert loops
+  constexpr int DPT = (kMaxM + BT - 1) / BT;   // departments per thread
+  constexpr int kTW = PS::TW;
+  int32_t *s_ids = sm.ids, *s_dep = sm.dep, *s_scan = sm.scan, *s_nd = sm.nd, *s_tmp = sm.tmp;
+  uint32_t *s_etok = sm.etok, *s_dtok = sm.dtok;
+  const int tid = threadIdx.x;
+  const int T = a.T, n = a.n, m = a.m, k = a.k, E = a.E;
+  const int tw = (T + 31) / 32;
+  const bool slice = a.plan == PLAN_SLICE;
+  const bool exp_slots = slice && a.d_p > 0;
+  const bool has_priv = a.plan == PLAN_FACTORED || a.d_p > 0;
+  const bool has_se = a.d_se > 0;
+  const int S = a.max_slots;
+  gmem<int32_t> *dept_count = glob(a.r.dept_count), *exp_count = glob(a.r.exp_count);
+  gmem<int32_t> *dept_offset = glob(a.r.dept_offset), *exp_offset = glob(a.r.exp_offset);
+  gmem<int32_t> *dept_tokens = glob(a.r.dept_tokens), *exp_tokens = glob(a.r.exp_tokens);
+  gmem<int32_t> *slot_pair = glob(a.slot_pair), *tok_exp_pair = glob(a.tok_exp_pair);
+  gmem<int32_t> *exp_src = glob(a.exp_src), *pair_dept = glob(a.pair_dept);
+  gmem<PlanCounts> *counts = glob(a.counts);
+  for (int i = tid; i < n * kTW; i += BT) s_etok[i] = 0;
+  for (int i = tid; i < m * kTW; i += BT) s_dtok[i] = 0;
+  lds_barrier();
+  for (int idx = tid; idx < T * k; idx += BT) {
+    const int t = idx / k;
+    const uint32_t bit = 1u << (t & 31);
+    const int e = LDS_IN ? s_ids[idx] : glob(a.r.topk_ids)[idx];
+    const int j = LDS_IN ? s_dep[idx] : glob(a.r.tok_depts)[idx];
+    if (!LDS_IN) {
+      s_ids[idx] = e;
+      s_dep[idx] = j;
+    }
+    atomicOr(&s_etok[e * kTW + (t >> 5)], bit);
+    if (j >= 0) atomicOr(&s_dtok[j * kTW + (t >> 5)], bit);
+  }
+  if (!LDS_IN)
+    for (int t = tid; t < T; t += BT) s_nd[t] = glob(a.r.tok_ndept)[t];
+  lds_barrier();
+
+  // counts
+  int my_dc[DPT] = {}, my_ec[EPT] = {};
+#pragma unroll
+  for (int q = 0; q < DPT; ++q) {
+    const int j = tid + q * BT;
+    if (j < m) {
+      int c = 0;
+      for (int w = 0; w < tw; ++w) c += __popc(s_dtok[j * kTW + w]);
+      my_dc[q] = c;
+      dept_count[j] = c;
+      s_scan[j] = c | ((c > 0) << 16);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    const int e = tid + q * BT;
+    if (e < n) {
+      int c = 0;
+      for (int w = 0; w < tw; ++w) c += __popc(s_etok[e * kTW + w]);
+      my_ec[q] = c;
+      exp_count[e] = c;
+      s_scan[m + e] = c | ((has_priv && c > 0) << 16);
+    }
+  }
+  lds_barrier();
+  const int tot = block_exscan(s_scan, m + n, s_tmp);
+  const int ndp = s_scan[m] & 0xffff, ud = s_scan[m] >> 16;
+  const int nep = (tot & 0xffff) - ndp, ue = (tot >> 16) - ud;
+  const int nep_priv = has_priv ? nep : 0;
+  auto doff = [&](int j) { return s_scan[j] & 0xffff; };
+  auto eoff = [&](int e) { return (s_scan[m + e] & 0xffff) - ndp; };
+  for (int j = tid; j < m; j += BT) dept_offset[j] = doff(j);
+  for (int e = tid; e < n; e += BT) exp_offset[e] = eoff(e);
+  if (tid == 0) {
+    dept_offset[m] = ndp;
+    exp_offset[n] = nep;
+  }
+  // every (token, rank) pair places itself: the expert of that rank and, for
+  // ranks below the token's department count, the department of that slot
+  for (int idx = tid; idx < T * k; idx += BT) {
+    const int t = idx / k, q = idx - t * k;
+    const int e = s_ids[idx];
+    const int pe = eoff(e) + rank_below(s_etok + e * kTW, t);
+    exp_tokens[pe] = t;
+    if (a.plan) {
+      tok_exp_pair[idx] = pe;
+      if (exp_slots) slot_pair[(size_t)t * S + s_nd[t] + q] = ndp + pe;
+      if (a.plan == PLAN_FACTORED) {
+        const int j = e / E;
+        exp_src[pe] = doff(j) + rank_below(s_dtok + j * kTW, t);
+      }
+    }
+    const int j = s_dep[idx];
+    if (j >= 0) {
+      const int pd = doff(j) + rank_below(s_dtok + j * kTW, t);
+      dept_tokens[pd] = t;
+      if (a.plan) slot_pair[(size_t)t * S + q] = pd;
+      if (a.plan == PLAN_FACTORED) pair_dept[pd] = j;
+    }
+  }
+  if (!a.plan) return;
+  if (has_se)
+    for (int t = tid; t < T; t += BT)
+      slot_pair[(size_t)t * S + s_nd[t] + (exp_slots ? k : 0)] = ndp + (slice ? nep_priv : 0) + t;
+
+  // unit tables: unit index of an active department / expert = number of
+  // active ones before it.  A unit's work items are its row-tile items times
+  // its token groups (wave_tokens tokens each).  Item prefixes over the units
+  // in table order are closed forms while no unit has more than one group;
+  // otherwise they come from block scans over an array with every
+  // department's items, then every expert's (the expert bitmaps' LDS, free
+  // after the placement above).
+  const int wb = a.w_bytes, ab = a.act_f32 ? 4 : 2;
+  const char *x = static_cast<const char *>(a.x);
+  auto wptr = [&](const void *base, int idx, int R, int C) -> const void * {
+    return static_cast<const char *>(base) + (size_t)idx * R * C * wb;
+  };
+  auto sptr = [&](const float *base, int idx, int R, int C) -> const float * {
+    if (!a.fp8) return nullptr;
+    return base + (size_t)idx * ((R + 127) / 128) * (C / 128);
+  };
+  const deamoe_weights &W = a.w;
+  // token groups of a unit: wave_tokens per group in the gate/up stages (pair
+  // A), wave_tokens_b in the separate down stages (pair B; the fused down
+  // kernel takes one group, and reads the bitmaps the item scans would reuse)
+  const int wt = a.wave_tokens, wtb = a.chain ? wt : a.wave_tokens_b;
+  const bool multi = T > min(wt, wtb);
+  auto groups = [&](int cnt) { return T > wt ? (cnt + wt - 1) / wt : 1; };
+  auto groups_b = [&](int cnt) { return T > wtb ? (cnt + wtb - 1) / wtb : 1; };
+  int32_t *s_ia = reinterpret_cast<int32_t *>(s_etok);           // [m + n] items, stage pair A
+  int32_t *s_ib = s_ia + kMaxM + kMaxN;                           // [m + n] items, stage pair B
+  const int dr = a.down_rows, dk = a.down_ks;
+  // items per row-tile item: (A dept, A expert, B dept, B expert)
+  int ia_d, ia_e, ib_d, ib_e;
+  if (slice) {
+    const int gd = tiles_per_item(a.d_s, dr, dk), gp = a.d_p ? tiles_per_item(a.d_p, dr, dk) : 1;
+    ia_d = (a.d_s + kTile - 1) / kTile;
+    ia_e = has_priv ? (a.d_p + kTile - 1) / kTile : 0;
+    ib_d = items_of(a.h, gd, dr);
+    ib_e = has_priv ? items_of(a.h, gp, dr) : 0;
+  } else {
+    const int d = a.d_s;
+    const int gd = tiles_per_item(d, dr, dk), g2 = tiles_per_item(d, dr, dk);
+    ia_d = (d + kTile - 1) / kTile;   // stage 0: W_g, W_u
+    ia_e = ia_d;                      // stage 1: A_g, A_u
+    ib_d = items_of(a.h, gd, dr);     // stage 3: W_d^T
+    ib_e = items_of(d, g2, dr);       // stage 2: A_d^T
+  }
+  int tot_a = 0, tot_b = 0;
+  static_assert(PS::MAXT >= kMaxT || PS::MAXT <= kTile, "a plan for fewer tokens has one group per unit");
+  if (PS::MAXT > kTile && multi) {
+    lds_barrier();   // the expert bitmaps are no longer read
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+      const int j = tid + q * BT;
+      if (j < m) {
+        s_ia[j] = my_dc[q] > 0 ? ia_d * groups(my_dc[q]) : 0;
+        s_ib[j] = my_dc[q] > 0 ? ib_d * groups_b(my_dc[q]) : 0;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      const int e = tid + q * BT;
+      if (e < n) {
+        const bool act = has_priv && my_ec[q] > 0;
+        s_ia[m + e] = act ? ia_e * groups(my_ec[q]) : 0;
+        s_ib[m + e] = act ? ib_e * groups_b(my_ec[q]) : 0;
+      }
+    }
+    lds_barrier();
+    const int2 tot = block_exscan2(s_ia, s_ib, m + n, s_tmp);
+    tot_a = tot.x;
+    tot_b = tot.y;
+  } else {
+    tot_a = ud * ia_d + ue * ia_e;
+    tot_b = ud * ib_d + ue * ib_e;
+  }
+  // first item of department j / expert e (unit index uj / ue_e) in each pair
+  const bool scanned = PS::MAXT > kTile && multi;
+  auto dbeg_a = [&](int j, int uj) { return scanned ? s_ia[j] : uj * ia_d; };
+  auto dbeg_b = [&](int j, int uj) { return scanned ? s_ib[j] : uj * ib_d; };
+  auto ebeg_a = [&](int e, int ui) { return scanned ? s_ia[m + e] : ud * ia_d + ui * ia_e; };
+  auto ebeg_b = [&](int e, int ui) { return scanned ? s_ib[m + e] : ud * ib_d + ui * ib_e; };
+  const int dept_a = scanned ? s_ia[m] : ud * ia_d;   // items of all departments
+  const int dept_b = scanned ? s_ib[m] : ud * ib_d;
+  const int kstep = a.w_bytes == 4 ? 64 : 128;   // K step of the weight type
+  if (slice) {
+    const int gd = tiles_per_item(a.d_s, dr, dk), gp = a.d_p ? tiles_per_item(a.d_p, dr, dk) : 1;
+    const int gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
+    const int bse = items_of(a.h, gse, dr);
+    // fused down stage (T <= 32): the units' K steps are concatenated in
+    // table order (departments, experts, the shared expert)
+    const int sd = a.d_s / kstep, sp = a.d_p / kstep;
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+      const int j = tid + q * BT, dc = my_dc[q];
+      if (j >= m || dc == 0) continue;
+      const int u = s_scan[j] >> 16, off = doff(j);
+      const int32_t *idx = a.r.dept_tokens + off;
+      char *ao = static_cast<char *>(a.abuf_dept) + (size_t)off * a.d_s * ab;
+      put_unit(glob(a.units[0]) + u, wptr(W.dept_gate, j, a.d_s, a.h), wptr(W.dept_up, j, a.d_s, a.h),
+               sptr(W.scale[0], j, a.d_s, a.h), sptr(W.scale[1], j, a.d_s, a.h), x, x, idx, ao,
+               nullptr, a.d_s, a.h, a.h, a.d_s, dc, dbeg_a(j, u), EPI_SWIGLU, a.act_f32);
+      if (a.chain)
+        put_chain(glob(a.cunits) + u, wptr(W.dept_down, j, a.h, a.d_s),
+                  sptr(W.scale[2], j, a.h, a.d_s), ao, a.wdense + (size_t)j * kChainT, a.d_s,
+                  s_dtok[j * kTW], u * sd);
+      else
+        put_unit(glob(a.units[1]) + u, wptr(W.dept_down, j, a.h, a.d_s), nullptr,
+                 sptr(W.scale[2], j, a.h, a.d_s), nullptr, ao, ao, nullptr,
+                 a.partial + (size_t)off * a.h, nullptr, a.h, a.d_s, a.d_s, a.h, dc,
+                 dbeg_b(j, u), EPI_STORE, 1, gd);
+    }
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      const int e = tid + q * BT;
+      if (!has_priv || e >= n || my_ec[q] == 0) continue;
+      const int ui = (s_scan[m + e] >> 16) - ud, u = ud + ui, off = eoff(e);
+      const int32_t *idx = a.r.exp_tokens + off;
+      char *ao = static_cast<char *>(a.abuf_exp) + (size_t)off * a.d_p * ab;
+      put_unit(glob(a.units[0]) + u, wptr(W.priv_gate, e, a.d_p, a.h), wptr(W.priv_up, e, a.d_p, a.h),
+               sptr(W.scale[3], e, a.d_p, a.h), sptr(W.scale[4], e, a.d_p, a.h), x, x, idx, ao,
+               nullptr, a.d_p, a.h, a.h, a.d_p, my_ec[q], ebeg_a(e, ui), EPI_SWIGLU,
+               a.act_f32);
+      if (a.chain)
+        put_chain(glob(a.cunits) + u, wptr(W.priv_down, e, a.h, a.d_p),
+                  sptr(W.scale[5], e, a.h, a.d_p), ao, a.wdense + (size_t)(m + e) * kChainT, a.d_p,
+                  s_etok[e * kTW], ud * sd + ui * sp);
+      else
+        put_unit(glob(a.units[1]) + u, wptr(W.priv_down, e, a.h, a.d_p), nullptr,
+                 sptr(W.scale[5], e, a.h, a.d_p), nullptr, ao, ao, nullptr,
+                 a.partial + (size_t)(ndp + off) * a.h, nullptr, a.h, a.d_p, a.d_p, a.h,
+                 my_ec[q], ebeg_b(e, ui), EPI_STORE, 1, gp);
+    }
+    // weight 1 of the shared expert: the row after the experts'
+    if (a.chain && tid < kChainT) glob(a.wdense)[(size_t)(m + n) * kChainT + tid] = 1.0f;
+    if (tid == 0) {
+      int units = ud + ue, items_a = tot_a, items_b = tot_b;
+      int steps = ud * sd + ue * sp;
+      if (has_se) {
+        put_unit(glob(a.units[0]) + units, W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
+                 sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
+                 a.h, a.d_se, T, items_a, EPI_SWIGLU, a.act_f32);
+        if (a.chain) {
+          put_chain(glob(a.cunits) + units, W.se_down, sptr(W.scale[8], 0, a.h, a.d_se), a.abuf_se,
+                    a.wdense + (size_t)(m + n) * kChainT, a.d_se,
+                    T >= 32 ? 0xffffffffu : (1u << T) - 1u, steps);
+          steps += a.d_se / kstep;
+        } else {
+          put_unit(glob(a.units[1]) + units, W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
+                   nullptr, a.abuf_se, a.abuf_se, nullptr,
+                   a.partial + (size_t)(ndp + nep_priv) * a.h, nullptr, a.h, a.d_se, a.d_se, a.h,
+                   T, items_b, EPI_STORE, 1, gse);
+        }
+        items_a += (a.d_se + kTile - 1) / kTile * groups(T);
+        items_b += bse * groups_b(T);
+        ++units;
+      }
+      counts->stage[0][0] = units;
+      counts->stage[0][1] = items_a;
+      counts->stage[1][0] = units;
+      counts->stage[1][1] = a.chain ? steps : items_b;
+    }
+  } else {  // PLAN_FACTORED
+    const int d = a.d_s;
+    const int gd = tiles_per_item(d, dr, dk), gse = a.d_se ? tiles_per_item(a.d_se, dr, dk) : 1;
+    const int bse = items_of(a.h, gse, dr);
+    const int g2 = tiles_per_item(d, dr, dk);   // A_d^T: d x d, streamed like the down projections
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+      const int j = tid + q * BT, dc = my_dc[q];
+      if (j >= m || dc == 0) continue;
+      const int u = s_scan[j] >> 16, off = doff(j);
+      const int32_t *idx = a.r.dept_tokens + off;
+      char *go = static_cast<char *>(a.gbuf) + (size_t)off * d * ab;
+      char *uo = static_cast<char *>(a.ubuf) + (size_t)off * d * ab;
+      char *zs = static_cast<char *>(a.zsbuf) + (size_t)off * d * ab;
+      put_unit(glob(a.units[0]) + u, wptr(W.dept_gate, j, d, a.h), wptr(W.dept_up, j, d, a.h),
+               sptr(W.scale[0], j, d, a.h), sptr(W.scale[1], j, d, a.h), x, x, idx, go, uo, d,
+               a.h, a.h, d, dc, dbeg_a(j, u), EPI_SIGMA2, a.act_f32);
+      if (a.chain)   // Z already carries the routing weights: unit weight 1
+        put_chain(glob(a.cunits) + u, wptr(W.dept_down, j, a.h, d), sptr(W.scale[2], j, a.h, d), zs,
+                  a.wdense + (size_t)(m + n) * kChainT, d, s_dtok[j * kTW], u * (d / kstep));
+      else
+        put_unit(glob(a.units[3]) + u, wptr(W.dept_down, j, a.h, d), nullptr,
+                 sptr(W.scale[2], j, a.h, d), nullptr, zs, zs, nullptr,
+                 a.partial + (size_t)off * a.h, nullptr, a.h, d, d, a.h, dc, dbeg_b(j, u),
+                 EPI_STORE, 1, gd);
+    }
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      const int e = tid + q * BT;
+      if (e >= n || my_ec[q] == 0) continue;
+      const int u = (s_scan[m + e] >> 16) - ud, off = eoff(e);
+      char *yo = static_cast<char *>(a.ybuf) + (size_t)off * d * ab;
+      put_unit(glob(a.units[1]) + u, wptr(W.priv_gate, e, d, d), wptr(W.priv_up, e, d, d),
+               sptr(W.scale[3], e, d, d), sptr(W.scale[4], e, d, d), a.gbuf, a.ubuf,
+               a.exp_src + off, yo, nullptr, d, d, d, d, my_ec[q], ebeg_a(e, u) - dept_a,
+               EPI_SWIGLU, a.act_f32);
+      put_unit(glob(a.units[2]) + u, wptr(W.priv_down, e, d, d), nullptr, sptr(W.scale[5], e, d, d),
+               nullptr, yo, yo, nullptr, a.zbuf + (size_t)off * d, nullptr, d, d, d, d,
+               my_ec[q], ebeg_b(e, u) - dept_b, EPI_SIGMA, 1, g2);
+    }
+    if (a.chain && tid < kChainT) glob(a.wdense)[(size_t)(m + n) * kChainT + tid] = 1.0f;
+    if (tid == 0) {
+      int units0 = ud, items0 = dept_a, units3 = ud, items3 = dept_b;
+      int steps = ud * (d / kstep);
+      if (has_se) {
+        put_unit(glob(a.units[0]) + units0, W.se_gate, W.se_up, sptr(W.scale[6], 0, a.d_se, a.h),
+                 sptr(W.scale[7], 0, a.d_se, a.h), x, x, nullptr, a.abuf_se, nullptr, a.d_se, a.h,
+                 a.h, a.d_se, T, items0, EPI_SWIGLU, a.act_f32);
+        if (a.chain) {
+          put_chain(glob(a.cunits) + units3, W.se_down, sptr(W.scale[8], 0, a.h, a.d_se), a.abuf_se,
+                    a.wdense + (size_t)(m + n) * kChainT, a.d_se,
+                    T >= 32 ? 0xffffffffu : (1u << T) - 1u, steps);
+          steps += a.d_se / kstep;
+        } else {
+          put_unit(glob(a.units[3]) + units3, W.se_down, nullptr, sptr(W.scale[8], 0, a.h, a.d_se),
+                   nullptr, a.abuf_se, a.abuf_se, nullptr, a.partial + (size_t)ndp * a.h,
+                   nullptr, a.h, a.d_se, a.d_se, a.h, T, items3, EPI_STORE, 1, gse);
+        }
+        ++units0;
+        items0 += (a.d_se + kTile - 1) / kTile * groups(T);
+        ++units3;
+        items3 += bse * groups_b(T);
+      }
+      if (a.chain) items3 = steps;
+      counts->stage[0][0] = units0;
+      counts->stage[0][1] = items0;
+      counts->stage[1][0] = ue;
+      counts->stage[1][1] = tot_a - dept_a;
+      counts->stage[2][0] = ue;
+      counts->stage[2][1] = tot_b - dept_b;
+      counts->stage[3][0] = units3;
+      counts->stage[3][1] = items3;
+    }
+  }
+  if (tid == 0) {
+    counts->n_dept_pairs = ndp;
+    counts->n_exp_pairs = nep_priv;
+    counts->n_pairs = ndp + (slice ? nep_priv : 0) + (has_se ? T : 0);
+  }
 }
 
 }  // namespace deamoe

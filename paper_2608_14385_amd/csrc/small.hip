@@ -1,7 +1,9 @@
-// Batches of at most four tokens, SLICE form: routing (Eq. 2 and the
-// department bookkeeping of Sec. 3.2), the gate/up stage of every active
-// department, expert and the shared expert, and the unit table of the fused
-// down kernel, in one launch after the router product.
+// Batches of at most four tokens: routing (Eq. 2 and the department
+// bookkeeping of Sec. 3.2), the plan of the later stages and the first
+// expert stage (SLICE: every active department's, expert's and the shared
+// expert's gate/up pair with SwiGLU; FACTORED: every active department's
+// W_g, W_u with sigma, and the shared expert) in one launch after the router
+// product.
 //
 // Every workgroup routes the tokens itself from the router's partial logits
 // (one wave per token, results in LDS only) and derives its own work item
@@ -11,15 +13,15 @@
 // workgroups the chip holds at once, so the routing is paid once per
 // workgroup rather than once per tile; with long tiles each workgroup
 // streams one, and the hardware hands a finishing workgroup's place to the
-// next tile.  The units are ordered as the plan kernel orders them:
-// active departments ascending, then active experts ascending, then the
+// next tile.  The units are ordered as the plan orders them: active
+// departments ascending, then (SLICE) active experts ascending, then the
 // shared expert; a unit's member tokens are in ascending order and its
-// gate/up output rows start at the unit's CSR offset, the sum of the member
-// counts of the units of its kind before it.  Workgroup 0 publishes the
-// routing (ids, weights, department lists, CSR lists, counts) and the fused
-// down kernel's units; workgroup 1 + w streams 16-row tile w (PERSIST: and
-// w + gridDim.x - 1, ...) of the step's gate/up pairs.  No workgroup reads
-// anything another one of this launch writes.
+// output rows start at the unit's CSR offset, the sum of the member counts
+// of the units of its kind before it.  Workgroup 0 publishes the routing and
+// runs the plan (CSR lists, counts, the unit tables of the later stages,
+// combine slots); workgroup 1 + w streams tile w (PERSIST: and
+// w + gridDim.x - 1, ...).  No workgroup reads anything another one of this
+// launch writes.
 #include <algorithm>
 #include <atomic>
 
@@ -34,9 +36,6 @@ static_assert(kSmallEW <= kWave && kSmallDW <= kWave, "bitmap words per wave");
 
 struct SmallSmem {
   uint32_t db[kSmallT][kSmallDW];      // departments of token t
-  int32_t ids[kSmallT * kMaxK];        // [t][rank] selected expert
-  int32_t dep[kSmallT * kMaxK];        // [t][slot] departments, -1 padded
-  int32_t nd[kSmallT];
   uint32_t eb[kSmallT][kSmallEW];      // selected experts of token t
   uint32_t pd[kSmallT][kSmallDW];      // exclusive word prefix of popc(department bitmap of t)
   uint32_t pe[kSmallT][kSmallEW];      // the same for eb[t]
@@ -62,13 +61,19 @@ __device__ inline int wave_select(const uint32_t *bits, const uint32_t *pre, int
   return 32 * w + __ffs(v) - 1;
 }
 
-// The per-token routing scratch lives in the weight staging space, which is
-// free until the first tile streams; the bitmaps that locate the tiles stay
-// beside it.
+// The routing scratch (and workgroup 0's plan) lives in the weight staging
+// space, which is free until the first tile streams; the bitmaps that locate
+// the tiles stay beside it.
+using SmallPlan = PlanSmemT<kSmallT>;
 template <int WT>
 union SmallLds {
   typename TileRunner<WT, 2, 1, 4>::Smem run;
   TokSmem tsm[kSmallT];
+  struct {
+    TokSmem tsm[kSmallT];
+    SmallPlan plan;
+    RouteArgs sa;
+  } pl;
 };
 
 template <int WT, int NS, bool PERSIST>
@@ -84,10 +89,20 @@ void small_route_gate_up_kernel(RouteArgs a) {
   const int T = a.T, m = a.m, n = a.n, k = a.k;
   const int dwords = (m + 31) / 32, ewords = (n + 31) / 32;
 
+  if (planner) {   // routing published, then the plan
+    args_to_lds<256>(a, lds.pl.sa);
+    if (wave < T)
+      route_one<NS>(a, wave, lane, lds.pl.tsm[wave],
+                    PlanIn{lds.pl.plan.ids, lds.pl.plan.dep, lds.pl.plan.nd, nullptr}, true);
+    lds_barrier();
+    plan_body<256, true>(lds.pl.sa, lds.pl.plan);
+    return;
+  }
+
   // 1. routing: wave t routes token t
   if (wave < T)
-    route_one<NS>(a, wave, lane, tsm[wave],
-                  PlanIn{ps.ids, ps.dep, ps.nd, ps.eb[wave]}, planner);
+    route_one<NS>(a, wave, lane, tsm[wave], PlanIn{nullptr, nullptr, nullptr, ps.eb[wave]},
+                  false);
   lds_barrier();
 
   // 2. unions of the tokens' department and expert bitmaps, word prefixes
@@ -126,10 +141,10 @@ void small_route_gate_up_kernel(RouteArgs a) {
   }
   lds_barrier();
 
-  const bool has_priv = a.d_p > 0, has_se = a.d_se > 0;
+  const bool slice = a.plan == PLAN_SLICE;
+  const bool has_priv = slice && a.d_p > 0, has_se = a.d_se > 0;
   const int ud = uniform(ps.nud), ue = has_priv ? uniform(ps.nue) : 0;
   const int wb = a.w_bytes, ab = a.act_f32 ? 4 : 2, h = a.h;
-  const int kstep = wb == 4 ? 64 : 128;
   const char *x = static_cast<const char *>(a.x);
   const deamoe_weights &W = a.w;
   auto wptr = [&](const void *base, int i, int R, int C) -> const void * {
@@ -160,146 +175,83 @@ void small_route_gate_up_kernel(RouteArgs a) {
     return o;
   };
 
-  if (!planner) {
-    // 3. this workgroup's 16-row tiles of the gate/up pairs
-    const int ia_d = (a.d_s + kTile - 1) / kTile, ia_e = (a.d_p + kTile - 1) / kTile;
-    const int ia_se = has_se ? (a.d_se + kTile - 1) / kTile : 0;
-    const int total = ud * ia_d + ue * ia_e + ia_se;
-    int32_t *idx = s_idx[wave];
-    auto stream_tile = [&](int item) {
-      GemmUnit U = {};
-      uint32_t mt;
-      if (item < ud * ia_d) {
-        const int u = item / ia_d;
-        item -= u * ia_d;
-        const int j = wave_select(ps.ud, ps.pud, dwords, u);
-        mt = dept_members(j);
-        const int off = dept_off(j);
-        U.w0 = wptr(W.dept_gate, j, a.d_s, h);
-        U.w1 = wptr(W.dept_up, j, a.d_s, h);
-        U.s0 = sptr(W.scale[0], j, a.d_s, h);
-        U.s1 = sptr(W.scale[1], j, a.d_s, h);
-        U.out0 = static_cast<char *>(a.abuf_dept) + (size_t)off * a.d_s * ab;
-        U.R = a.d_s;
-        U.ldout = a.d_s;
-      } else if ((item -= ud * ia_d) < ue * ia_e) {
-        const int u = item / ia_e;
-        item -= u * ia_e;
-        const int e = wave_select(ps.ue, ps.pue, ewords, u);
-        mt = exp_members(e);
-        const int off = exp_off(e);
-        U.w0 = wptr(W.priv_gate, e, a.d_p, h);
-        U.w1 = wptr(W.priv_up, e, a.d_p, h);
-        U.s0 = sptr(W.scale[3], e, a.d_p, h);
-        U.s1 = sptr(W.scale[4], e, a.d_p, h);
-        U.out0 = static_cast<char *>(a.abuf_exp) + (size_t)off * a.d_p * ab;
-        U.R = a.d_p;
-        U.ldout = a.d_p;
-      } else {
-        item -= ue * ia_e;   // the shared expert
-        mt = (1u << T) - 1u;
-        U.w0 = W.se_gate;
-        U.w1 = W.se_up;
-        U.s0 = sptr(W.scale[6], 0, a.d_se, h);
-        U.s1 = sptr(W.scale[7], 0, a.d_se, h);
-        U.out0 = a.abuf_se;
-        U.R = a.d_se;
-        U.ldout = a.d_se;
+  // 3. this workgroup's 16-row tiles of the first stage
+  const int ia_d = (a.d_s + kTile - 1) / kTile, ia_e = has_priv ? (a.d_p + kTile - 1) / kTile : 0;
+  const int ia_se = has_se ? (a.d_se + kTile - 1) / kTile : 0;
+  const int total = ud * ia_d + ue * ia_e + ia_se;
+  int32_t *idx = s_idx[wave];
+  auto stream_tile = [&](int item) {
+    GemmUnit U = {};
+    uint32_t mt;
+    int sigma = DEAMOE_SIGMA_SILU;
+    U.epi = EPI_SWIGLU;
+    if (item < ud * ia_d) {
+      const int u = item / ia_d;
+      item -= u * ia_d;
+      const int j = wave_select(ps.ud, ps.pud, dwords, u);
+      mt = dept_members(j);
+      const size_t off = dept_off(j);
+      U.w0 = wptr(W.dept_gate, j, a.d_s, h);
+      U.w1 = wptr(W.dept_up, j, a.d_s, h);
+      U.s0 = sptr(W.scale[0], j, a.d_s, h);
+      U.s1 = sptr(W.scale[1], j, a.d_s, h);
+      if (slice) {
+        U.out0 = static_cast<char *>(a.abuf_dept) + off * a.d_s * ab;
+      } else {   // FACTORED: sigma(W_g x) and sigma(W_u x) kept apart
+        U.out0 = static_cast<char *>(a.gbuf) + off * a.d_s * ab;
+        U.out1 = static_cast<char *>(a.ubuf) + off * a.d_s * ab;
+        U.epi = EPI_SIGMA2;
+        sigma = a.sigma;
       }
-      // the unit's tokens in ascending order, in this wave's LDS slot (the
-      // previous tile's loads have all been issued: TileRunner ends with a
-      // workgroup barrier)
-      if (lane == 0) {
-        int i = 0;
-        for (int t = 0; t < T; ++t)
-          if ((mt >> t) & 1u) idx[i++] = t;
-      }
-      wave_lds_sync();
-      U.in0 = U.in1 = x;
-      U.idx = idx;
-      U.K = h;
-      U.ldw = h;
-      U.ldin = h;
-      U.ntok = __popc(mt);
-      U.epi = EPI_SWIGLU;
-      U.out_f32 = a.act_f32;
-      U.tpg = 1;
-      Run::run(lds.run, &U, item, true, DEAMOE_SIGMA_SILU);
-    };
-    if constexpr (PERSIST) {
-      for (int it = blockIdx.x - 1; it < total; it += gridDim.x - 1) stream_tile(it);
-    } else if ((int)blockIdx.x - 1 < total) {
-      stream_tile(blockIdx.x - 1);
+      U.R = a.d_s;
+      U.ldout = a.d_s;
+    } else if ((item -= ud * ia_d) < ue * ia_e) {
+      const int u = item / ia_e;
+      item -= u * ia_e;
+      const int e = wave_select(ps.ue, ps.pue, ewords, u);
+      mt = exp_members(e);
+      const size_t off = exp_off(e);
+      U.w0 = wptr(W.priv_gate, e, a.d_p, h);
+      U.w1 = wptr(W.priv_up, e, a.d_p, h);
+      U.s0 = sptr(W.scale[3], e, a.d_p, h);
+      U.s1 = sptr(W.scale[4], e, a.d_p, h);
+      U.out0 = static_cast<char *>(a.abuf_exp) + off * a.d_p * ab;
+      U.R = a.d_p;
+      U.ldout = a.d_p;
+    } else {
+      item -= ue * ia_e;   // the shared expert
+      mt = (1u << T) - 1u;
+      U.w0 = W.se_gate;
+      U.w1 = W.se_up;
+      U.s0 = sptr(W.scale[6], 0, a.d_se, h);
+      U.s1 = sptr(W.scale[7], 0, a.d_se, h);
+      U.out0 = a.abuf_se;
+      U.R = a.d_se;
+      U.ldout = a.d_se;
     }
-    return;
-  }
-
-  // 4. workgroup 0: CSR lists, counts and the fused down kernel's units
-  gmem<int32_t> *dept_count = glob(a.r.dept_count), *exp_count = glob(a.r.exp_count);
-  gmem<int32_t> *dept_offset = glob(a.r.dept_offset), *exp_offset = glob(a.r.exp_offset);
-  gmem<int32_t> *dept_tokens = glob(a.r.dept_tokens), *exp_tokens = glob(a.r.exp_tokens);
-  int ndp = 0;
-  for (int t = 0; t < T; ++t) ndp += ps.nd[t];
-  for (int j = tid; j < m; j += blockDim.x) {
-    dept_count[j] = __popc(dept_members(j));
-    dept_offset[j] = dept_off(j);
-  }
-  for (int e = tid; e < n; e += blockDim.x) {
-    exp_count[e] = __popc(exp_members(e));
-    exp_offset[e] = exp_off(e);
-  }
-  if (tid == 0) {
-    dept_offset[m] = ndp;
-    exp_offset[n] = T * k;
-  }
-  for (int i = tid; i < T * k; i += blockDim.x) {
-    const int t = i / k, q = i - t * k;
-    const uint32_t below = (1u << t) - 1u;
-    const int e = ps.ids[i];
-    exp_tokens[exp_off(e) + __popc(exp_members(e) & below)] = t;
-    if (q < ps.nd[t]) {
-      const int j = ps.dep[i];
-      dept_tokens[dept_off(j) + __popc(dept_members(j) & below)] = t;
+    // the unit's tokens in ascending order, in this wave's LDS slot (the
+    // previous tile's loads have all been issued: TileRunner ends with a
+    // workgroup barrier)
+    if (lane == 0) {
+      int i = 0;
+      for (int t = 0; t < T; ++t)
+        if ((mt >> t) & 1u) idx[i++] = t;
     }
-  }
-  const int sd = a.d_s / kstep, sp = a.d_p / kstep;
-  for (int j = tid; j < m; j += blockDim.x) {
-    if (!((ps.ud[j >> 5] >> (j & 31)) & 1u)) continue;
-    const int u = rank_pre(ps.ud, ps.pud, j);
-    char *ao = static_cast<char *>(a.abuf_dept) + (size_t)dept_off(j) * a.d_s * ab;
-    put_chain(glob(a.cunits) + u, wptr(W.dept_down, j, h, a.d_s), sptr(W.scale[2], j, h, a.d_s),
-              ao, a.wdense + (size_t)j * kChainT, a.d_s, dept_members(j), u * sd);
-  }
-  if (has_priv) {
-    for (int e = tid; e < n; e += blockDim.x) {
-      if (!((ps.ue[e >> 5] >> (e & 31)) & 1u)) continue;
-      const int ui = rank_pre(ps.ue, ps.pue, e);
-      char *ao = static_cast<char *>(a.abuf_exp) + (size_t)exp_off(e) * a.d_p * ab;
-      put_chain(glob(a.cunits) + ud + ui, wptr(W.priv_down, e, h, a.d_p),
-                sptr(W.scale[5], e, h, a.d_p), ao, a.wdense + (size_t)(m + e) * kChainT, a.d_p,
-                exp_members(e), ud * sd + ui * sp);
-    }
-  }
-  // weight 1 of the shared expert: the row after the experts'
-  if (tid < kChainT) glob(a.wdense)[(size_t)(m + n) * kChainT + tid] = 1.0f;
-  if (tid == 0) {
-    int units = ud + ue, steps = ud * sd + ue * sp;
-    int items = ud * ((a.d_s + kTile - 1) / kTile) + ue * ((a.d_p + kTile - 1) / kTile);
-    if (has_se) {
-      put_chain(glob(a.cunits) + units, W.se_down, sptr(W.scale[8], 0, h, a.d_se), a.abuf_se,
-                a.wdense + (size_t)(m + n) * kChainT, a.d_se, (1u << T) - 1u, steps);
-      steps += a.d_se / kstep;
-      items += (a.d_se + kTile - 1) / kTile;
-      ++units;
-    }
-    gmem<PlanCounts> *counts = glob(a.counts);
-    counts->stage[0][0] = units;
-    counts->stage[0][1] = items;
-    counts->stage[1][0] = units;
-    counts->stage[1][1] = steps;
-    counts->n_dept_pairs = ndp;
-    counts->n_exp_pairs = has_priv ? T * k : 0;
-    counts->n_pairs = ndp + (has_priv ? T * k : 0) + (has_se ? T : 0);
+    wave_lds_sync();
+    U.in0 = U.in1 = x;
+    U.idx = idx;
+    U.K = h;
+    U.ldw = h;
+    U.ldin = h;
+    U.ntok = __popc(mt);
+    U.out_f32 = a.act_f32;
+    U.tpg = 1;
+    Run::run(lds.run, &U, item, true, sigma);
+  };
+  if constexpr (PERSIST) {
+    for (int it = blockIdx.x - 1; it < total; it += gridDim.x - 1) stream_tile(it);
+  } else if ((int)blockIdx.x - 1 < total) {
+    stream_tile(blockIdx.x - 1);
   }
 }
 
@@ -353,12 +305,26 @@ static hipError_t launch_small_wt(const RouteArgs &a, int items, hipStream_t s) 
     case 2: return launch_small_ns<WT, 2>(a, items, s);
     case 4: return launch_small_ns<WT, 4>(a, items, s);
     case 8: return launch_small_ns<WT, 8>(a, items, s);
+    case 16: return launch_small_ns<WT, 16>(a, items, s);
     default: return hipErrorInvalidValue;
   }
 }
 
+// One-tile workgroups of this kernel an MI355X holds at once: 256 CUs, three
+// per CU for bf16 and fp32 weights (registers), four for fp8 (LDS).
+constexpr int kCUs = 256;
+static int single_tile_slots(int wtype) { return kCUs * (wtype == WT_FP8 ? 4 : 3) - 1; }
+
+bool small_route_pays(int wtype, int n, int h, int w_bytes, bool group_limited, int items) {
+  if (route_ns(n) > 16) return false;
+  if (!group_limited) return true;                     // set-only top-k: a short prologue
+  if ((size_t)2 * kTile * h * w_bytes < kPersistTileBytes) return true;   // routes once
+  const int slots = single_tile_slots(wtype);          // (nearly) every tile in one round
+  return items <= slots + slots / 8;
+}
+
 hipError_t launch_small_route_gate_up(const RouteArgs &a, int wtype, int items, hipStream_t s) {
-  if (a.T < 1 || a.T > kSmallT || a.plan != PLAN_SLICE || !a.chain || route_ns(a.n) > 8)
+  if (a.T < 1 || a.T > kSmallT || a.plan == PLAN_NONE || route_ns(a.n) > 16)
     return hipErrorInvalidValue;
   switch (wtype) {
     case WT_F32: return launch_small_wt<WT_F32>(a, items, s);

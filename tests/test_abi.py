@@ -274,12 +274,16 @@ def test_trace_points():
         [4, 4, 5, 5, 5, 5, 6, 6]
     s7 = D.make_config(W.PRESETS["7b_bf16"].layer, 64)     # h 2048: fused up to 4 tokens
     assert [D.deamoe_trace_points(s7, T) for T in (1, 4, 5, 16)] == [4, 4, 6, 6]
-    # routers of more than 512 experts keep the separate routing kernel
-    assert D.deamoe_trace_points(cfg_c3(n_experts=1024, n_depts=32), 1) == 5
+    # routers of more than 1024 experts keep the separate routing kernel
+    assert D.deamoe_trace_points(cfg_c3(n_experts=2048, n_depts=32), 1) == 5
     f = D.make_config(W.PRESETS["dsv3_factored"].layer, 64)
-    assert [D.deamoe_trace_points(f, T) for T in (1, 16, 17)] == [8, 8, 9]
+    # group-limited routing with long tiles routes inside the first stage
+    # only while (nearly) all of its tiles fit in one round (one token here)
+    assert [D.deamoe_trace_points(f, T) for T in (1, 2, 4, 5, 16, 17)] == [7, 8, 8, 8, 8, 9]
     q = D.make_config(W.PRESETS["qwen3_factored"].layer, 64)   # h 4096: separate stages
-    assert [D.deamoe_trace_points(q, T) for T in (1, 16)] == [9, 9]
+    assert [D.deamoe_trace_points(q, T) for T in (1, 16)] == [8, 9]
+    k2 = D.make_config(W.PRESETS["kimik2_factored"].layer, 64)   # 1280 experts
+    assert D.deamoe_trace_points(k2, 1) == 8
     # more active units than the fused kernel's table holds: separate stages
     big = cfg_c3(n_experts=2048, n_depts=64, top_k=32)
     assert [D.deamoe_trace_points(big, T) for T in (8, 16)] == [5, 6]

@@ -59,18 +59,23 @@ def test_small_variants(variant):
     of at most four tokens, which route inside the gate/up launch."""
     T = 9
     if variant == "t3_group_limited":
-        return check_case(Case(small(n_experts=64, n_depts=8, top_k=6, top_k_dept=3), 3, seed=11))
+        check_case(Case(small(n_experts=64, n_depts=8, top_k=6, top_k_dept=3), 3, seed=11))
+        return
     if variant == "t2_shared_expert":
-        return check_case(Case(small(d_shared_expert=192, renorm=False), 2, seed=12))
+        check_case(Case(small(d_shared_expert=192, renorm=False), 2, seed=12))
+        return
     if variant == "t4_zipf_sigmoid_scaled":
-        return check_case(Case(small(score="sigmoid", route_scale=2.5), 4, seed=13, bias="zipf"))
+        check_case(Case(small(score="sigmoid", route_scale=2.5), 4, seed=13, bias="zipf"))
+        return
     if variant == "t1_strict_cover":
-        return check_case(Case(small(n_experts=64, n_depts=8, top_k=6, top_k_dept=3,
+        check_case(Case(small(n_experts=64, n_depts=8, top_k=6, top_k_dept=3,
                                      dept_cover=1), 1, seed=14))
+        return
     if variant == "t3_fp8":
-        return check_case(Case(small(hidden=512, d_shared=512, d_private=256, score="sigmoid",
+        check_case(Case(small(hidden=512, d_shared=512, d_private=256, score="sigmoid",
                                      w_dtype="fp8", act_dtype="bf16", top_k=3,
                                      d_shared_expert=128), 3, seed=15))
+        return
     if variant == "uniform_logits":
         case = Case(small(), 16, seed=1, logits="uniform")
     elif variant == "zipf_bias":
@@ -142,9 +147,28 @@ def test_tiny_factored(T):
     check_case(Case(P["tiny_factored"].layer, T, seed=10 + T))
 
 
-@pytest.mark.parametrize("variant", ["sigma_none", "identity_private", "group_limited_se"])
+@pytest.mark.parametrize("variant", ["sigma_none", "identity_private", "group_limited_se",
+                                     "t3_gelu", "t2_rmsnorm_se", "t4_fp8_group_limited",
+                                     "t3_strict_cover"])
 def test_factored_variants(variant):
+    """FACTORED variants; the t<N> cases are batches of at most four tokens,
+    which route and plan inside the department gate/up launch."""
     base = P["tiny_factored"].layer
+    if variant == "t3_gelu":
+        check_case(Case(base.replace(sigma="gelu"), 3, seed=120))
+        return
+    if variant == "t2_rmsnorm_se":
+        check_case(Case(base.replace(sigma="rmsnorm", d_shared_expert=128), 2, seed=121))
+        return
+    if variant == "t4_fp8_group_limited":
+        check_case(Case(base.replace(w_dtype="fp8", act_dtype="bf16", n_experts=32,
+                                            n_depts=4, top_k=5, top_k_dept=2, score="sigmoid",
+                                            d_shared_expert=128), 4, seed=122))
+        return
+    if variant == "t3_strict_cover":
+        check_case(Case(base.replace(n_experts=32, n_depts=4, top_k=5, top_k_dept=2,
+                                            dept_cover=1), 3, seed=123))
+        return
     if variant == "sigma_none":
         case = Case(base.replace(sigma="none"), 7, seed=20)
     elif variant == "identity_private":
@@ -153,6 +177,15 @@ def test_factored_variants(variant):
         case = Case(base.replace(n_experts=32, n_depts=4, top_k=5, top_k_dept=2,
                                  d_shared_expert=128, score="sigmoid"), 11, seed=22)
     check_case(case)
+
+
+@pytest.mark.parametrize("T", [2, 3])
+def test_many_departments(T):
+    """640 departments of two experts behind a 1280-expert router: at most
+    four tokens then route and plan in one 256-thread workgroup, whose
+    threads each cover several departments."""
+    cfg = small(n_experts=1280, n_depts=640, top_k=4, d_shared=128, d_private=64)
+    check_case(Case(cfg, T, seed=130 + T))
 
 
 @pytest.mark.parametrize("T", [1, 4, 40])
