@@ -177,7 +177,7 @@ int ntt_of(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
 // runs at three waves per SIMD, which outweighs streaming the rows of a
 // unit with more than 16 tokens once per group.
 int wave_ntt_of(const deamoe_config &c, int T) {
-  if (DEAMOE_FACTORED_NTT1 && c.form == DEAMOE_FORM_FACTORED) return 1;
+  if (c.form == DEAMOE_FORM_FACTORED) return 1;
   return T <= kTile ? 1 : 2;
 }
 int token_groups_max(const deamoe_config &c, int T) {
@@ -203,21 +203,27 @@ int down_groups_max(const deamoe_config &c, int T) {
 // Waves sharing one SLICE gate/up tile: four, and two above 32 tokens, where
 // two token tiles leave two waves per SIMD and twice the tiles in flight per
 // workgroup stream faster.
-int slice_gate_up_ks_of(int T) { return T > DEAMOE_SGU_KS4_MAX_T ? 2 : 4; }
+int slice_gate_up_ks_of(int T) { return T > kChainT ? 2 : 4; }
 
-// Rows of a down-projection tile: row pairs while the token tiles are few
-// enough for both halves' accumulators to stay in registers.
-int down_rows_of(int) { return DEAMOE_DOWN_PAIR ? 2 * kTile : kTile; }
+// K split of the FACTORED stages: the department gate/up over 4 waves, the
+// private gate/up (split token operands) over 2 (4 was slower at every batch).
+constexpr int kFactoredGateUpKs = 4, kFactoredPrivKs = 2;
+
+// Down-projection tiles are row pairs: two adjacent 16-row tiles of a matrix
+// streamed by one wave with one token operand for both.
+constexpr int kDownRows = 2 * kTile;
 
 // Waves sharing one down-projection tile.  The SLICE form packs several
-// short private tiles per work item and keeps whole tiles per wave; the
-// FACTORED form (every contraction d long) splits K while the batch leaves
+// short private tiles per work item and keeps whole tiles per wave (K split
+// over two waves up to two tokens, where the batch leaves few work items);
+// the FACTORED form (every contraction d long) splits K four ways up to 8
+// tokens and two ways up to 32 (64 where h >= 4096), while the batch leaves
 // too few tiles to occupy the waves.
 int down_ks_of(const deamoe_config &c, int T) {
-  if (c.form == DEAMOE_FORM_SLICE) return T <= DEAMOE_SDOWN_KS2_T ? 2 : DEAMOE_KS_DOWN;
-  if (T <= DEAMOE_FDOWN_KS4_T) return 4;
+  if (c.form == DEAMOE_FORM_SLICE) return T <= 2 ? 2 : 1;
+  if (T <= 8) return 4;
   const bool wide = c.hidden >= 4096;
-  return T <= DEAMOE_FDOWN_KS2_T || (wide && T <= DEAMOE_FDOWN_KS2_WIDE_T) ? 2 : 1;
+  return T <= 32 || (wide && T <= 64) ? 2 : 1;
 }
 
 
@@ -231,12 +237,9 @@ int down_ks_of(const deamoe_config &c, int T) {
 // a few long contractions that the split-K stage already streams well, and
 // the fused kernel gains only with a grid of at least kChainMinTilesFactored
 // workgroups (measured on the 7168- and 4096-wide Table 1 layers).
-#ifndef DEAMOE_CHAIN
-#define DEAMOE_CHAIN 1
-#endif
 constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 192;
 bool use_chain(const deamoe_config &c, int T) {
-  if (!DEAMOE_CHAIN || T > kChainT) return false;
+  if (T > kChainT) return false;
   // the plan builds the fused kernel's units for one token group only
   if (token_groups_max(c, T) > 1) return false;
   const int tiles = c.hidden / (2 * kTile);
@@ -341,7 +344,7 @@ void fill_route_args(RouteArgs &a, const deamoe_config &c, int T, const void *x,
   a.w_bytes = wbytes_of(c.w_dtype);
   a.fp8 = c.w_dtype == DEAMOE_FP8_E4M3_B128;
   a.plan = plan;
-  a.down_rows = down_rows_of(T);
+  a.down_rows = kDownRows;
   a.down_ks = down_ks_of(c, T);
   a.wave_tokens = kTile * wave_ntt_of(c, T);
   a.wave_tokens_b = kTile * down_ntt_of(c, T);
@@ -424,13 +427,11 @@ bool routing_complete(const deamoe_routing &r) {
 }
 
 
-// Launch of a down-projection stage.
-hipError_t launch_down(const GemmStage &st, int wt, int T, int ntt, int groups, int ks,
-                       int units_max, int R, int cap, hipStream_t s) {
-  const int rows = down_rows_of(T);
-  const bool pair = rows == 2 * kTile;
-  return launch_grouped_gemm(st, wt, pair ? 2 : 1, pair ? GEMM_PAIR : GEMM_PLAIN, ntt, ks,
-                             tiles_bound(units_max, R, rows) * groups, cap, s);
+// Launch of a down-projection stage (row-pair tiles).
+hipError_t launch_down(const GemmStage &st, int wt, int ntt, int groups, int ks, int units_max,
+                       int R, int cap, hipStream_t s) {
+  return launch_grouped_gemm(st, wt, 2, GEMM_PAIR, ntt, ks,
+                             tiles_bound(units_max, R, kDownRows) * groups, cap, s);
 }
 
 constexpr int kGridCap = 8192;   // 256 CUs x 32 workgroups
@@ -502,14 +503,14 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
       return DEAMOE_OK;
     }
     const int units = act_depts + (c.d_private ? act_exps : 0) + se;
-    DEAMOE_TRY(launch_down(stage(1), wt, T, down_ntt_of(c, T), down_groups_max(c, T),
+    DEAMOE_TRY(launch_down(stage(1), wt, down_ntt_of(c, T), down_groups_max(c, T),
                            down_ks_of(c, T), units, c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
   } else {
     const int d = c.d_shared;
     const int t0 = tiles_bound(act_depts, d) + se * tiles_bound(1, c.d_shared_expert);
     if (!small)
-      DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, DEAMOE_KS_FGU, t0 * groups,
+      DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, kFactoredGateUpKs, t0 * groups,
                                      kGridCap, s));
     if (c.sigma == DEAMOE_SIGMA_RMSNORM) {   // timed with stage 0
       RowNormArgs na;
@@ -521,10 +522,10 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
       DEAMOE_TRY(launch_rownorm(na, T * dk, s));
     }
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, DEAMOE_KS_FPRIV,
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, kFactoredPrivKs,
                                    tiles_bound(act_exps, d) * groups, kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_down(stage(2), wt, T, ntt, groups, down_ks_of(c, T), act_exps, d,
+    DEAMOE_TRY(launch_down(stage(2), wt, ntt, groups, down_ks_of(c, T), act_exps, d,
                            kGridCap, s));
     DEAMOE_TRY(ev.mark());
     ZsumArgs za;
@@ -556,7 +557,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
       DEAMOE_TRY(ev.mark());
       return DEAMOE_OK;
     }
-    DEAMOE_TRY(launch_down(stage(3), wt, T, ntt, groups, down_ks_of(c, T), act_depts + se,
+    DEAMOE_TRY(launch_down(stage(3), wt, ntt, groups, down_ks_of(c, T), act_depts + se,
                            c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
   }

@@ -222,7 +222,9 @@ streamed:
 template <int WT, int NTT>
 static hipError_t launch_chain_wt(const ChainArgs &a, hipStream_t s) {
   const dim3 grid((a.h + 2 * kTile - 1) / (2 * kTile));
-  constexpr int KSC = DEAMOE_CHAIN_WAVES, PF = DEAMOE_CHAIN_PF;
+  // 8 waves per workgroup, each streaming one contiguous range of the
+  // concatenated K steps, one load group in flight while one is multiplied
+  constexpr int KSC = 8, PF = 1;
   hipLaunchKernelGGL((chain_down_kernel<WT, NTT, KSC, PF>), grid, dim3(KSC * kWave), 0, s, a);
   return hipGetLastError();
 }

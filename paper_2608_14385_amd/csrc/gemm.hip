@@ -120,17 +120,11 @@ static hipError_t dispatch_ks(const GemmStage &st, int mode, int ntt, int ks, in
 
 hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int mode, int ntt,
                                int ks, int max_tiles, int grid_cap, hipStream_t s) {
-  if (nw == 2) {
-    switch (wtype) {
-      case WT_F32: return dispatch_ks<WT_F32, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
-      case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
-      default: return dispatch_ks<WT_FP8, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
-    }
-  }
+  if (nw != 2) return hipErrorInvalidValue;   // every stage streams two matrices or a row pair
   switch (wtype) {
-    case WT_F32: return dispatch_ks<WT_F32, 1>(st, 0, ntt, ks, max_tiles, grid_cap, s);
-    case WT_BF16: return dispatch_ks<WT_BF16, 1>(st, 0, ntt, ks, max_tiles, grid_cap, s);
-    default: return dispatch_ks<WT_FP8, 1>(st, 0, ntt, ks, max_tiles, grid_cap, s);
+    case WT_F32: return dispatch_ks<WT_F32, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
+    case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
+    default: return dispatch_ks<WT_FP8, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
   }
 }
 

@@ -384,18 +384,12 @@ __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int tok0, int si
 // item per token group of 16 * NTT tokens and tile item; the items of one
 // tile item are 8 * TPB apart, in workgroups on the same XCD.
 // SPLIT: the two matrices read different token operands (in0 / in1).
-#ifndef DEAMOE_PF_NW1
-#define DEAMOE_PF_NW1 1
-#endif
-#ifndef DEAMOE_PF_NW2
-#define DEAMOE_PF_NW2 1
-#endif
 template <int WT, int NW, int NTT, int KS, bool SPLIT = false, bool PAIR = false>
 struct TileRunner {
   static constexpr int TR = PAIR ? 2 * kTile : kTile;   // weight rows of a tile
   static constexpr int TPB = 4 / KS;
-  // load groups in flight per wave
-  static constexpr int PF = NTT > 2 ? 1 : (NW == 1 ? DEAMOE_PF_NW1 : DEAMOE_PF_NW2);
+  // load groups in flight per wave while one is multiplied
+  static constexpr int PF = 1;
   static constexpr int STAGE_BYTES = NW * WLoad<WT>::REGION;   // per wave
   static constexpr int RED_BYTES = KS > 1 ? NW * NTT * kWave * 16 : 0;   // per wave
   static constexpr int WAVE_BYTES = STAGE_BYTES > RED_BYTES ? STAGE_BYTES : RED_BYTES;

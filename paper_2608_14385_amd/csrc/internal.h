@@ -13,63 +13,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// K split of the down-projection stages (1: one wave per work item of
-// several row tiles; 2 or 4: the waves of a workgroup share one row tile).
-#ifndef DEAMOE_KS_DOWN
-#define DEAMOE_KS_DOWN 1
-#endif
-
-// Down-projection stages stream two adjacent 16-row tiles of a matrix per
-// wave (one token operand for both) for up to 32 tokens; 0 always streams
-// single tiles.
-#ifndef DEAMOE_DOWN_PAIR
-#define DEAMOE_DOWN_PAIR 1
-#endif
-
-// SLICE down projections split K over 2 waves up to this many tokens (more
-// waves in flight while the batch leaves few work items).
-#ifndef DEAMOE_SDOWN_KS2_T
-#define DEAMOE_SDOWN_KS2_T 2
-#endif
-// SLICE gate/up stages split K over 4 waves up to this many tokens, over 2
-// above.
-#ifndef DEAMOE_SGU_KS4_MAX_T
-#define DEAMOE_SGU_KS4_MAX_T 32
-#endif
-// K split of the FACTORED department gate/up stage (W_g x, W_u x).
-#ifndef DEAMOE_KS_FGU
-#define DEAMOE_KS_FGU 4
-#endif
-// K split of the FACTORED private gate/up stage (A_g G, A_u U).
-#ifndef DEAMOE_KS_FPRIV
-#define DEAMOE_KS_FPRIV 2
-#endif
-// FACTORED down-projection stages split K four ways up to this many tokens,
-// two ways up to the next (up to the third for hidden sizes of 4096 and up).
-#ifndef DEAMOE_FDOWN_KS4_T
-#define DEAMOE_FDOWN_KS4_T 8
-#endif
-#ifndef DEAMOE_FDOWN_KS2_T
-#define DEAMOE_FDOWN_KS2_T 32
-#endif
-#ifndef DEAMOE_FDOWN_KS2_WIDE_T
-#define DEAMOE_FDOWN_KS2_WIDE_T 64
-#endif
-
-// FACTORED stages take one token tile per wave at every batch (0: two tiles
-// from 17 tokens on, as SLICE).
-#ifndef DEAMOE_FACTORED_NTT1
-#define DEAMOE_FACTORED_NTT1 1
-#endif
-// Fused SLICE down stage: waves per workgroup (each streams one contiguous
-// range of the concatenated K steps) and load groups in flight per wave.
-#ifndef DEAMOE_CHAIN_WAVES
-#define DEAMOE_CHAIN_WAVES 8
-#endif
-#ifndef DEAMOE_CHAIN_PF
-#define DEAMOE_CHAIN_PF 1
-#endif
-
 constexpr int kWave = 64;
 constexpr int kTile = 16;   // MFMA tile edge: 16 weight rows x 16 tokens
 

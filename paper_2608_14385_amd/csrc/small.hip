@@ -79,7 +79,7 @@ union SmallLds {
 template <int WT, int NS, bool PERSIST>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
 void small_route_gate_up_kernel(RouteArgs a) {
-  using Run = TileRunner<WT, 2, 1, 4>;
+  using Run = TileRunner<WT, 2, 1, 4>;   // four waves share a tile's K steps
   __shared__ SmallLds<WT> lds;
   __shared__ SmallSmem ps;
   __shared__ int32_t s_idx[kSmallT][kSmallT];   // per wave: member tokens of its unit
