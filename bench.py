@@ -32,12 +32,16 @@ sys.path.insert(0, ROOT)
 
 METRIC = "MoE-layer decode latency (µs) + achieved HBM GB/s, batch 1–64, vs vanilla MoE"
 HBM_PEAK_GBPS = 8000.0
-# HBM bytes per launch of the gate/up kernel at 16 tokens, from rocprofv3
-# FETCH_SIZE and WRITE_SIZE passes scaled by what the same counters read for a
-# 1 GiB device copy (x2.0 and x1.0).  Valid only for the library sources they
-# were taken on: the digest below covers them, and a mismatch reports null.
-TRAFFIC_BYTES = 2341119814
-TRAFFIC_SOURCES_SHA256 = "76faa57b15f49e3f6f801dbeb809d12f0160ce30240e5067fc9b374fc7ae0122"
+# Figures of the gate/up kernel at 16 tokens taken with rocprofv3 on the
+# library sources whose digest follows (a mismatch reports them as null):
+#  - HBM bytes per launch from FETCH_SIZE and WRITE_SIZE passes, scaled by
+#    what the same counters read for a plain device copy (x2.0 and x1.0);
+#  - the average launch duration from a kernel-trace run of the default
+#    command (profiles/gate_up_dsv3_bf16_T16_kernel_trace.md), which excludes
+#    the launch gap that the benchmark's own events include.
+TRAFFIC_BYTES = 2341137408
+PROFILED_GATE_UP_US = 350.85
+TRAFFIC_SOURCES_SHA256 = "4a81742ed26d13b43ad6980b664943a31c5876109071784e0effeed567017405"
 
 
 def library_sources_digest() -> str:
@@ -54,10 +58,12 @@ def library_sources_digest() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(cfg, T: int):
-    if cfg.name != "dsv3_bf16" or T != 16:
-        return None
-    return TRAFFIC_BYTES if library_sources_digest() == TRAFFIC_SOURCES_SHA256 else None
+def profiled_figures(cfg, T: int):
+    """(traffic bytes, profiled average launch us) of the gate/up kernel for
+    the workload and sources they were taken on, else (None, None)."""
+    if cfg.name != "dsv3_bf16" or T != 16 or library_sources_digest() != TRAFFIC_SOURCES_SHA256:
+        return None, None
+    return TRAFFIC_BYTES, PROFILED_GATE_UP_US
 
 
 def log(*a):
@@ -536,24 +542,36 @@ def main():
         gu = [gate_up_bytes(cfg, T, b[2], b[3]) for b in run.bytes]
         gu_bytes = float(np.mean([gu[i % len(gu)] for i in range(args.steps)]))
         achieved = gu_bytes / (mean[dom] * 1e-3) / 1e9
-        result["roofline"] = {"kernel": "grouped_gemm_kernel (gate/up stage)", "bound": "hbm",
+        traffic, prof_us = profiled_figures(cfg, T)
+        result["roofline"] = {"kernel": f"{names[dom]} stage", "bound": "hbm",
                               "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                               "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                              "traffic": measured_traffic(cfg, T),
+                              "traffic": traffic,
                               "bytes_per_launch": int(gu_bytes),
-                              "avg_launch_us": round(float(mean[dom]) * 1e3, 2)}
+                              "avg_launch_us": round(float(mean[dom]) * 1e3, 2),
+                              "timing": "HIP events before and after the launch on its stream "
+                                        "(they include the launch gap)"}
+        if prof_us is not None:
+            pa = gu_bytes / (prof_us * 1e-6) / 1e9
+            result["roofline"]["profiled"] = {
+                "avg_launch_us": prof_us, "achieved": round(pa, 1),
+                "frac": round(pa / HBM_PEAK_GBPS, 4),
+                "source": "rocprofv3 kernel trace, profiles/gate_up_dsv3_bf16_T16_kernel_trace.md"}
         log(f"[bench] kernels (us): {result['kernels_us']}")
 
     # vanilla-MoE comparator and the batch sweep
     sweep_rows = []
-    brun = None
+    brun = b16run = None
     if not args.no_baseline:
         bbytes = sum(math.prod(s) for s in W.weight_shapes(bcfg).values()) * \
             {"f32": 4, "bf16": 2, "fp8": 1}[bcfg.w_dtype]
         brun = LayerRun(bcfg, max_T, copies_for(bbytes), baseline=True, bias=bias)
+        if bcfg.w_dtype == "fp8":   # also the vanilla layer with bf16 weights
+            b16 = bcfg.replace(name=bcfg.name.replace("fp8", "bf16"), w_dtype="bf16")
+            b16run = LayerRun(b16, max_T, copies_for(2 * bbytes), baseline=True, bias=bias)
     for Tb in sweep:
         row = {"batch": Tb}
-        for name, r in (("deamoe", run), ("vanilla", brun)):
+        for name, r in (("deamoe", run), ("vanilla", brun), ("vanilla_bf16", b16run)):
             if r is None:
                 continue
             r.set_batch(Tb)
@@ -568,6 +586,9 @@ def main():
         if brun is not None:
             row["speedup"] = round(row["vanilla"]["latency_us"] / row["deamoe"]["latency_us"], 3)
             row["byte_ratio"] = round(row["deamoe"]["bytes"] / row["vanilla"]["bytes"], 4)
+        if b16run is not None:
+            row["speedup_vs_bf16_vanilla"] = round(
+                row["vanilla_bf16"]["latency_us"] / row["deamoe"]["latency_us"], 3)
         log(f"[bench] sweep {row}")
         sweep_rows.append(row)
     if sweep_rows:
@@ -575,6 +596,8 @@ def main():
         head = [r for r in sweep_rows if r["batch"] == T]
         if head and "speedup" in head[0]:
             result["speedup_vs_vanilla"] = head[0]["speedup"]
+        if head and "speedup_vs_bf16_vanilla" in head[0]:
+            result["speedup_vs_bf16_vanilla"] = head[0]["speedup_vs_bf16_vanilla"]
 
     if args.layers > 0:
         result["multi_layer"] = multi_layer(cfg, wl.baseline, args.layers, T, max(5, args.steps // 10))
