@@ -488,7 +488,7 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
                    se * tiles_bound(1, c.d_shared_expert);
     if (!small)
       DEAMOE_TRY(launch_grouped_gemm(stage(0), wt, 2, GEMM_PLAIN, ntt, slice_gate_up_ks_of(T),
-                                     ta * groups, kGridCap, s));
+                                     ta * groups, kGridCap, s, c.hidden < 4096));
     DEAMOE_TRY(ev.mark());
     if (use_chain(c, T)) {   // down projections and combine in one kernel
       ChainArgs ch;

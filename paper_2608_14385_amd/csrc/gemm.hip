@@ -9,9 +9,9 @@ namespace deamoe {
 
 constexpr int kMaxUnitsCached = 4096;
 
-template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR>
+template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR, bool B1>
 __device__ __attribute__((always_inline)) void grouped_gemm_body(const GemmStage &st) {
-  using Run = TileRunner<WT, NW, NTT, KS, SPLIT, PAIR>;
+  using Run = TileRunner<WT, NW, NTT, KS, SPLIT, PAIR, B1>;
   __shared__ typename Run::Smem sm;
   __shared__ int32_t s_begin[kMaxUnitsCached];
   const int n_units = st.counts[0], n_tiles = st.counts[1];
@@ -39,92 +39,93 @@ __device__ __attribute__((always_inline)) void grouped_gemm_body(const GemmStage
 
 template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR>
 __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
-  grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR>(st);
+  grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR, false>(st);
 }
 
-// The same at three waves per SIMD (at most 168 registers).  Left alone the
-// compiler gives two-matrix stages with split token operands (the FACTORED
-// private gate/up) 166 registers, two waves per SIMD; with one token tile,
-// three (no spills) keep the 640 workgroups of a one-token step resident in
-// one round.
-template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR>
+// The same at three waves per SIMD (at most 168 registers), for the
+// instantiations that fit them without spilling:
+//  - the split-operand stage with one token tile (the FACTORED private
+//    gate/up, which the compiler left alone gives 166 registers, two waves
+//    per SIMD; three keep the 640 workgroups of a one-token step resident in
+//    one round);
+//  - fp8 stages with two token tiles;
+//  - bf16 and fp32 stages with two token tiles whose token operand is
+//    requested per step (B1): row pairs (same-process A/B at the DeepSeek-V3
+//    shape, down stage at 128 tokens 378.3 -> 370.0 us, skewed 178.9 ->
+//    172.8), and gate/up pairs of layers narrower than 4096 (the 7B-class
+//    layer 48.5 -> 44.9 us at 32 tokens, 52.3 -> 48.5 at 64; at the
+//    DeepSeek-V3 shape they were 0-2 % slower, so two waves stay there).
+template <int WT, int NW, int NTT, int KS, bool SPLIT, bool PAIR, bool B1>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
 void grouped_gemm_occ3_kernel(GemmStage st) {
-  grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR>(st);
+  grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR, B1>(st);
 }
 
-// fp8 stages with two token tiles also fit three waves without spilling
-// (bf16 ones would spill, which costs far more than the occupancy gains).
-template <int WT, int NTT>
-constexpr bool occ3_two_tiles() { return NTT == 2 && WT == WT_FP8; }
-
-// mode: GemmMode; row pairs exist for NTT <= 2 only (the host picks them so)
+// mode: GemmMode; row pairs exist for NTT <= 2 only (the host picks them so).
+// narrow: two-token-tile gate/up pairs run at three waves per SIMD.
 template <int WT, int NW, int NTT, int KS>
 static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int grid_cap,
-                              hipStream_t s) {
+                              bool narrow, hipStream_t s) {
   constexpr int TPB = 4 / KS;
   int grid = (max_tiles + TPB - 1) / TPB;
   grid = grid < 1 ? 1 : (grid > grid_cap ? grid_cap : grid);
+  constexpr bool FP8 = WT == WT_FP8;
+  auto plain = [&](auto k) {
+    hipLaunchKernelGGL(k, dim3(grid), dim3(256), 0, s, st);
+    return hipGetLastError();
+  };
   if constexpr (NW == 2) {
-    if (mode == 1) {
+    if (mode == GEMM_SPLIT) {
       if constexpr (NTT == 1 && KS > 1)
-        hipLaunchKernelGGL((grouped_gemm_occ3_kernel<WT, NW, NTT, KS, true, false>), dim3(grid),
-                           dim3(256), 0, s, st);
+        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, true, false, false>);
       else   // two token tiles (or no K split) would spill at three waves per SIMD
-        hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, true, false>), dim3(grid),
-                           dim3(256), 0, s, st);
-      return hipGetLastError();
+        return plain(grouped_gemm_kernel<WT, NW, NTT, KS, true, false>);
     }
-    if (mode == 2) {
-      if constexpr (NTT <= 2) {   // row pairs are built for up to two token tiles
-        if constexpr (occ3_two_tiles<WT, NTT>())
-          hipLaunchKernelGGL((grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, true>), dim3(grid),
-                             dim3(256), 0, s, st);
-        else
-          hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false, true>), dim3(grid),
-                             dim3(256), 0, s, st);
-        return hipGetLastError();
-      }
-      return hipErrorInvalidValue;
+    if (mode == GEMM_PAIR) {
+      if constexpr (NTT == 2)
+        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, true, !FP8>);
+      else if constexpr (NTT == 1)
+        return plain(grouped_gemm_kernel<WT, NW, NTT, KS, false, true>);
+      return hipErrorInvalidValue;   // row pairs are built for up to two token tiles
+    }
+    if constexpr (NTT == 2 && KS > 1) {
+      if constexpr (FP8)
+        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, false, false>);
+      else if (narrow)
+        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, false, true>);
     }
   }
-  if constexpr (NW == 2 && occ3_two_tiles<WT, NTT>())
-    hipLaunchKernelGGL((grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, false>), dim3(grid),
-                       dim3(256), 0, s, st);
-  else
-    hipLaunchKernelGGL((grouped_gemm_kernel<WT, NW, NTT, KS, false, false>), dim3(grid),
-                       dim3(256), 0, s, st);
-  return hipGetLastError();
+  return plain(grouped_gemm_kernel<WT, NW, NTT, KS, false, false>);
 }
 
 // Token tiles per wave: 1 or 2 (larger token sets are split into groups).
 template <int WT, int NW, int KS>
 static hipError_t dispatch_ntt(const GemmStage &st, int mode, int ntt, int max_tiles, int cap,
-                               hipStream_t s) {
+                               bool narrow, hipStream_t s) {
   switch (ntt) {
-    case 1: return launch_gemm<WT, NW, 1, KS>(st, mode, max_tiles, cap, s);
-    case 2: return launch_gemm<WT, NW, 2, KS>(st, mode, max_tiles, cap, s);
+    case 1: return launch_gemm<WT, NW, 1, KS>(st, mode, max_tiles, cap, narrow, s);
+    case 2: return launch_gemm<WT, NW, 2, KS>(st, mode, max_tiles, cap, narrow, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int WT, int NW>
 static hipError_t dispatch_ks(const GemmStage &st, int mode, int ntt, int ks, int max_tiles,
-                              int cap, hipStream_t s) {
+                              int cap, bool narrow, hipStream_t s) {
   switch (ks) {
-    case 1: return dispatch_ntt<WT, NW, 1>(st, mode, ntt, max_tiles, cap, s);
-    case 2: return dispatch_ntt<WT, NW, 2>(st, mode, ntt, max_tiles, cap, s);
-    default: return dispatch_ntt<WT, NW, 4>(st, mode, ntt, max_tiles, cap, s);
+    case 1: return dispatch_ntt<WT, NW, 1>(st, mode, ntt, max_tiles, cap, narrow, s);
+    case 2: return dispatch_ntt<WT, NW, 2>(st, mode, ntt, max_tiles, cap, narrow, s);
+    default: return dispatch_ntt<WT, NW, 4>(st, mode, ntt, max_tiles, cap, narrow, s);
   }
 }
 
 hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int mode, int ntt,
-                               int ks, int max_tiles, int grid_cap, hipStream_t s) {
+                               int ks, int max_tiles, int grid_cap, hipStream_t s, bool narrow) {
   if (nw != 2) return hipErrorInvalidValue;   // every stage streams two matrices or a row pair
   switch (wtype) {
-    case WT_F32: return dispatch_ks<WT_F32, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
-    case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
-    default: return dispatch_ks<WT_FP8, 2>(st, mode, ntt, ks, max_tiles, grid_cap, s);
+    case WT_F32: return dispatch_ks<WT_F32, 2>(st, mode, ntt, ks, max_tiles, grid_cap, narrow, s);
+    case WT_BF16: return dispatch_ks<WT_BF16, 2>(st, mode, ntt, ks, max_tiles, grid_cap, narrow, s);
+    default: return dispatch_ks<WT_FP8, 2>(st, mode, ntt, ks, max_tiles, grid_cap, narrow, s);
   }
 }
 

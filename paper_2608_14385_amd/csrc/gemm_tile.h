@@ -191,7 +191,12 @@ __device__ inline void stage_weights(char *lds, const u32x4 (&Gb)[NW][WLoad<WT>:
 // row instead of weights, so every iteration issues the same loads.
 // `done(rt, acc)` is called (and acc cleared) after the last K step of
 // each tile when nsub > 1; with nsub == 1 the caller finishes the tile.
-template <int WT, int NW, int NTT, bool SPLIT, int PF, bool PAIR, bool NT, class Done>
+// B1: the token operand is requested with the step that uses it rather than
+// PF steps ahead (one buffer instead of PF + 1), before that step's weight
+// prefetch, so that waiting for it never waits for the prefetch; its L2
+// round trip overlaps the weights of the step in flight.  This saves the
+// registers of PF token-operand buffers.
+template <int WT, int NW, int NTT, bool SPLIT, int PF, bool PAIR, bool NT, bool B1, class Done>
 __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, int ks, int tok0,
                                  char *lds, f32x4 (&acc)[NW][NTT], Done done) {
   static_assert(!PAIR || (NW == 2 && !SPLIT), "a row pair is two tiles of one matrix");
@@ -243,13 +248,19 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
     if constexpr (NW == 2) scw[1] = gfptr(PAIR ? U.s0 : U.s1)[e];
   }
   u32x4 G[NB][NW][LD::NQ];
-  u32x4 B[NB][NTT][BV];
+  u32x4 B[B1 ? 1 : NB][NTT][BV];
   int SC[NB];   // fp8: window entry of the group's scales
-  // issue the load group of virtual step v (tile v / nloc, K step kp + (v % nloc) * ks)
+  // K step of virtual step v (tile v / nloc, K step kp + (v % nloc) * ks)
+  auto kstep_of = [&](int v) {
+    const bool ok = v < total;
+    const int sub = ok ? v / nloc : 0;
+    return ok ? kp + (v - sub * nloc) * ks : 0;
+  };
+  // issue the weight loads (and, without B1, the token operand) of virtual step v
   auto issue = [&](u32x4(&Gb)[NW][LD::NQ], u32x4(&Bb)[NTT][BV], int &sc, int v) {
     const bool ok = v < total;
     const int sub = ok ? v / nloc : 0;
-    const int kstep = ok ? kp + (v - sub * nloc) * ks : 0;
+    const int kstep = kstep_of(v);
 #pragma unroll
     for (int q = 0; q < LD::NQ; ++q) {
       const int row = min((rt0 + sub) * TR + q * LD::RPI + lrow, rmax);
@@ -259,7 +270,7 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
         Gb[n][q] = NT ? __builtin_nontemporal_load(gptr(ok ? (n ? w1 : w0) + woff : dummy))
                       : *gptr(ok ? (n ? w1 : w0) + woff : dummy);
     }
-    load_b<WT, NTT, SPLIT>(Bb, bp0, bp1, ntt, (size_t)kstep * ASEG, g);
+    if constexpr (!B1) load_b<WT, NTT, SPLIT>(Bb, bp0, bp1, ntt, (size_t)kstep * ASEG, g);
     if constexpr (WT == WT_FP8)   // a row pair lies in one scale row
       sc = uniform((((rt0 + sub) * TR) / 128 - srow0) * sblocks + kstep);
   };
@@ -267,12 +278,16 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
     stage_weights<WT, NW>(lds, Gb, a);
   };
 #pragma unroll
-  for (int p = 0; p < PF; ++p) issue(G[p], B[p], SC[p], p);
+  for (int p = 0; p < PF; ++p) issue(G[p], B[B1 ? 0 : p], SC[p], p);
   for (int v = 0;;) {
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
       const int qn = (q + NB - 1) % NB;   // the buffer consumed one step ago
-      issue(G[qn], B[qn], SC[qn], v + PF);
+      if constexpr (B1) {
+        load_b<WT, NTT, SPLIT>(B[0], bp0, bp1, ntt, (size_t)kstep_of(v) * ASEG, g);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      issue(G[qn], B[B1 ? 0 : qn], SC[qn], v + PF);
       __builtin_amdgcn_sched_barrier(0);
       u32x4 a[NW][4];
       stage(G[q], a);
@@ -282,7 +297,7 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
         for (int n = 0; n < NW; ++n)
           sc[n] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scw[n]), SC[q]));
       }
-      step_mma<WT, NW, NTT, SPLIT>(a, B[q], ntt, sc, acc);
+      step_mma<WT, NW, NTT, SPLIT>(a, B[B1 ? 0 : q], ntt, sc, acc);
       __builtin_amdgcn_sched_barrier(0);
       ++v;
       if (nsub > 1 && v % nloc == 0) {   // a tile of a multi-tile work item is complete
@@ -384,7 +399,9 @@ __device__ inline void tile_epilogue(const GemmUnit &U, int rt, int tok0, int si
 // item per token group of 16 * NTT tokens and tile item; the items of one
 // tile item are 8 * TPB apart, in workgroups on the same XCD.
 // SPLIT: the two matrices read different token operands (in0 / in1).
-template <int WT, int NW, int NTT, int KS, bool SPLIT = false, bool PAIR = false>
+// B1: the token operand is requested per step (see tile_loop), which lets
+// stages with two token tiles fit three waves per SIMD.
+template <int WT, int NW, int NTT, int KS, bool SPLIT = false, bool PAIR = false, bool B1 = false>
 struct TileRunner {
   static constexpr int TR = PAIR ? 2 * kTile : kTile;   // weight rows of a tile
   static constexpr int TPB = 4 / KS;
@@ -445,10 +462,10 @@ struct TileRunner {
       // groups of a tile item run on one XCD at about the same time); every
       // other weight row is read once and streams past them.
       if (groups > 1)
-        tile_loop<WT, NW, NTT, SPLIT, PF, PAIR, false>(*U, rt0, nsub, kp, KS, tok0, sm.buf[wave],
+        tile_loop<WT, NW, NTT, SPLIT, PF, PAIR, false, B1>(*U, rt0, nsub, kp, KS, tok0, sm.buf[wave],
                                                        acc, done);
       else
-        tile_loop<WT, NW, NTT, SPLIT, PF, PAIR, true>(*U, rt0, nsub, kp, KS, tok0, sm.buf[wave],
+        tile_loop<WT, NW, NTT, SPLIT, PF, PAIR, true, B1>(*U, rt0, nsub, kp, KS, tok0, sm.buf[wave],
                                                       acc, done);
     }
     if constexpr (KS > 1) {

@@ -118,9 +118,12 @@ enum GemmMode : int {
   GEMM_PAIR = 2,    // the "two matrices" are adjacent 16-row tiles of one matrix
 };
 // max_tiles bounds the stage's work items (row tiles of kTile rows, or of
-// 2 * kTile rows in GEMM_PAIR mode) for the grid size.
+// 2 * kTile rows in GEMM_PAIR mode) for the grid size.  narrow: a gate/up
+// stage of a layer narrower than 4096 (two token tiles then run at three
+// waves per SIMD).
 hipError_t launch_grouped_gemm(const GemmStage &st, int wtype, int nw, int mode, int ntt,
-                               int ks, int max_tiles, int grid_cap, hipStream_t s);
+                               int ks, int max_tiles, int grid_cap, hipStream_t s,
+                               bool narrow = false);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 // SLICE batches of 1..4 tokens with the fused down kernel (a.chain): routing,
 // the gate/up stage and the down kernel's units in one launch (items: the
