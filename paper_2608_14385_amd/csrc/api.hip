@@ -206,8 +206,15 @@ int down_groups_max(const deamoe_config &c, int T) {
 int slice_gate_up_ks_of(int T) { return T > kChainT ? 2 : 4; }
 
 // K split of the FACTORED stages: the department gate/up over 4 waves, the
-// private gate/up (split token operands) over 2 (4 was slower at every batch).
-constexpr int kFactoredGateUpKs = 4, kFactoredPrivKs = 2;
+// private gate/up (split token operands) over 2 (4 was slower at every
+// batch), or over none where its contraction (d) is shorter than 1024 and
+// more than 16 tokens give enough tiles (Baseline-7B, d = 384: 143.3 ->
+// 134.0 us per step at 64 tokens; even at 16; the wider Table 1 layers
+// were 1-2 % slower without the split).
+constexpr int kFactoredGateUpKs = 4;
+int factored_priv_ks_of(const deamoe_config &c, int T) {
+  return c.d_shared < 1024 && T > 16 ? 1 : 2;
+}
 
 // Down-projection tiles are row pairs: two adjacent 16-row tiles of a matrix
 // streamed by one wave with one token operand for both.
@@ -522,8 +529,9 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
       DEAMOE_TRY(launch_rownorm(na, T * dk, s));
     }
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt, kFactoredPrivKs,
-                                   tiles_bound(act_exps, d) * groups, kGridCap, s));
+    DEAMOE_TRY(launch_grouped_gemm(stage(1), wt, 2, GEMM_SPLIT, ntt,
+                                   factored_priv_ks_of(c, T), tiles_bound(act_exps, d) * groups,
+                                   kGridCap, s));
     DEAMOE_TRY(ev.mark());
     DEAMOE_TRY(launch_down(stage(2), wt, ntt, groups, down_ks_of(c, T), act_exps, d,
                            kGridCap, s));

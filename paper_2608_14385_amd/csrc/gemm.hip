@@ -45,9 +45,13 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
 // The same at three waves per SIMD (at most 168 registers), for the
 // instantiations that fit them without spilling:
 //  - the split-operand stage with one token tile (the FACTORED private
-//    gate/up, which the compiler left alone gives 166 registers, two waves
-//    per SIMD; three keep the 640 workgroups of a one-token step resident in
-//    one round);
+//    gate/up), its two token operands requested per step (B1): 138
+//    registers, where both operands double-buffered took 166 at two waves
+//    per SIMD, or 168 and a 24-byte spill at three.  Same-process A/B
+//    against the latter (outputs bit-identical): 745.6 -> 704.4 us per step
+//    at 16 tokens on the DeepSeek-V3 FACTORED layer (the stage 405.0 ->
+//    364.3), 2071.8 -> 1977.4 at 64, 148.4 -> 145.3 at one token; Kimi-K2
+//    879.6 -> 839.6, DeepSeek-V2 406.2 -> 391.6, Qwen3 330.8 -> 319.5 at 16;
 //  - fp8 stages with two token tiles;
 //  - bf16 and fp32 stages with two token tiles whose token operand is
 //    requested per step (B1): row pairs (same-process A/B at the DeepSeek-V3
@@ -76,9 +80,9 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
   };
   if constexpr (NW == 2) {
     if (mode == GEMM_SPLIT) {
-      if constexpr (NTT == 1 && KS > 1)
-        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, true, false, false>);
-      else   // two token tiles (or no K split) would spill at three waves per SIMD
+      if constexpr (NTT == 1)
+        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, true, false, true>);
+      else   // two token tiles would spill at three waves per SIMD (no stage uses them)
         return plain(grouped_gemm_kernel<WT, NW, NTT, KS, true, false>);
     }
     if (mode == GEMM_PAIR) {
