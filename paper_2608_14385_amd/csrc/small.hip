@@ -86,7 +86,7 @@ void small_route_gate_up_kernel(RouteArgs a) {
   TokSmem *tsm = lds.tsm;
   const int wave = uniform(threadIdx.x / kWave), lane = lane_id(), tid = threadIdx.x;
   const bool planner = blockIdx.x == 0;
-  const int T = a.T, m = a.m, n = a.n, k = a.k;
+  const int T = a.T, m = a.m, n = a.n;
   const int dwords = (m + 31) / 32, ewords = (n + 31) / 32;
 
   if (planner) {   // routing published, then the plan
@@ -255,10 +255,10 @@ void small_route_gate_up_kernel(RouteArgs a) {
   }
 }
 
-// Workgroups of a kernel the current device holds at once (0 if unknown),
+// Workgroups of kernel K the current device holds at once (0 if unknown),
 // queried once per device and kernel.
-template <class K>
-static int resident_workgroups(K kernel) {
+template <auto K>
+static int resident_workgroups() {
   constexpr int kDevices = 64;
   static std::atomic<int> cache[kDevices];
   int dev = 0;
@@ -266,7 +266,7 @@ static int resident_workgroups(K kernel) {
   int v = cache[dev].load(std::memory_order_relaxed);
   if (v == 0) {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, K, 256, 0) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return 0;
     v = per_cu * cus;
@@ -284,11 +284,11 @@ template <int WT, int NS>
 static hipError_t launch_small_ns(const RouteArgs &a, int items, hipStream_t s) {
   const size_t tile_bytes = (size_t)2 * kTile * a.h * a.w_bytes;
   if (tile_bytes < kPersistTileBytes &&
-      items >= resident_workgroups(small_route_gate_up_kernel<WT, NS, false>)) {
+      items >= resident_workgroups<small_route_gate_up_kernel<WT, NS, false>>()) {
     // one workgroup per tile up to what the chip holds at once (then each
     // streams several), plus the publishing workgroup
-    auto kernel = small_route_gate_up_kernel<WT, NS, true>;
-    const int slots = resident_workgroups(kernel) - 1;
+    constexpr auto kernel = small_route_gate_up_kernel<WT, NS, true>;
+    const int slots = resident_workgroups<kernel>() - 1;
     const int g = slots > 0 ? std::min(items, slots) : items;
     hipLaunchKernelGGL(kernel, dim3(1 + std::max(g, 1)), dim3(256), 0, s, a);
   } else {
