@@ -10,7 +10,8 @@
 // (P_{t,j} for a department, Sec. 3.2), one product over the concatenated K
 // steps of all units in which token t's column carries the weight p_{t,u}
 // and zero for units it does not use.  A workgroup owns 32 rows of y (two
-// 16-row halves sharing the token operand) and splits the concatenated K
+// 16-row halves sharing the token operand; 16 rows on narrow layers) and
+// splits the concatenated K
 // steps into KSC contiguous ranges, one per wave, so that every wave streams
 // one long run of weight rows; each K step's product is added to the
 // accumulator with the lane's token weight (times the fp8 block scale), and
@@ -23,13 +24,13 @@
 
 namespace deamoe {
 
-// One K step of both halves: the step's products start from zero and are
+// One K step of every half: the step's products start from zero and are
 // added with the per-lane factor f (the token's weight, times the fp8 scale).
-template <int WT, int NTT>
-__device__ inline void chain_mma(const u32x4 (&a)[2][4], const u32x4 (&b)[4], float f,
-                                 f32x4 (&acc)[2][NTT], int tt) {
+template <int WT, int NW, int NTT>
+__device__ inline void chain_mma(const u32x4 (&a)[NW][4], const u32x4 (&b)[4], float f,
+                                 f32x4 (&acc)[NW][NTT], int tt) {
 #pragma unroll
-  for (int n = 0; n < 2; ++n) {
+  for (int n = 0; n < NW; ++n) {
     f32x4 t = {0.f, 0.f, 0.f, 0.f};
     if constexpr (WT == WT_F32) {
 #pragma unroll
@@ -58,12 +59,12 @@ __device__ inline P *uniform_ptr(P *p) {
   return reinterpret_cast<P *>(((uint64_t)hi << 32) | lo);
 }
 
-template <int WT, int NTT, int KSC, int PF>
+// NW: 16-row halves of y per workgroup (1 or 2; two share the token operand).
+template <int WT, int NW, int NTT, int KSC, int PF>
 __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
   using Tr = WTraits<WT>;
   using LD = WLoad<WT>;
-  constexpr int NW = 2;            // the two 16-row halves of the tile
-  constexpr int TR = 2 * kTile;    // rows of y per workgroup
+  constexpr int TR = NW * kTile;   // rows of y per workgroup
   constexpr int NB = PF + 1;       // load groups per wave: PF in flight, one multiplied
   constexpr int ASEG = Tr::K_STEP * Tr::A_BYTES;
   constexpr int STAGE = NW * LD::REGION;
@@ -83,7 +84,7 @@ __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
   const int g = lane >> 4, j = lane & 15;
   const int T = a.T, R = a.h, rt = blockIdx.x;
   const int lrow = lane / LD::LPR, lchunk = lane % LD::LPR;
-  const int rmax = R - 1 - kTile;   // last row the first half may read
+  const int rmax = R - 1 - (NW - 1) * kTile;   // last row the first half may read
   const int s_lo = uniform((int)((int64_t)S * wave / KSC));
   const int total = uniform((int)((int64_t)S * (wave + 1) / KSC)) - s_lo;
   char *lds = s_buf[wave];
@@ -152,7 +153,8 @@ __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
         const size_t woff = (size_t)row * ldw * Tr::W_BYTES + (size_t)ck * LD::WSEG;
         const size_t half = (size_t)kTile * ldw * Tr::W_BYTES;
         Gb[0][q] = __builtin_nontemporal_load(gptr(ok ? w0 + woff : dummy));
-        Gb[1][q] = __builtin_nontemporal_load(gptr(ok ? w0 + woff + half : dummy));
+        if constexpr (NW == 2)
+          Gb[1][q] = __builtin_nontemporal_load(gptr(ok ? w0 + woff + half : dummy));
       }
 #pragma unroll
       for (int tt = 0; tt < NTT; ++tt) {
@@ -180,7 +182,7 @@ __global__ __launch_bounds__(KSC * kWave) void chain_down_kernel(ChainArgs a) {
           // tokens outside the unit have weight zero (their operand is a
           // member's row, so the product is finite)
           const float f0 = (MM[q][tt] >> lane) & 1 ? P[q][tt] : 0.f;
-          chain_mma<WT>(w, B[q][tt], WT == WT_FP8 ? f0 * SC[q] : f0, acc, tt);
+          chain_mma<WT, NW>(w, B[q][tt], WT == WT_FP8 ? f0 * SC[q] : f0, acc, tt);
         }
         __builtin_amdgcn_sched_barrier(0);
         if (++v >= total) goto streamed;
@@ -213,25 +215,36 @@ streamed:
       if (tok < T) {
         const size_t off = (size_t)tok * R + row0;
         if (row0 < R) store4(a.y, a.act_f32, off, acc[0][tt], row0 + 3 < R, R - row0);
-        if (row1 < R) store4(a.y, a.act_f32, off + kTile, acc[1][tt], row1 + 3 < R, R - row1);
+        if (NW == 2 && row1 < R)
+          store4(a.y, a.act_f32, off + kTile, acc[NW - 1][tt], row1 + 3 < R, R - row1);
       }
     }
   }
 }
 
-template <int WT, int NTT>
+template <int WT, int NW, int NTT>
 static hipError_t launch_chain_wt(const ChainArgs &a, hipStream_t s) {
-  const dim3 grid((a.h + 2 * kTile - 1) / (2 * kTile));
+  const dim3 grid((a.h + NW * kTile - 1) / (NW * kTile));
   // 8 waves per workgroup, each streaming one contiguous range of the
   // concatenated K steps, one load group in flight while one is multiplied
   constexpr int KSC = 8, PF = 1;
-  hipLaunchKernelGGL((chain_down_kernel<WT, NTT, KSC, PF>), grid, dim3(KSC * kWave), 0, s, a);
+  hipLaunchKernelGGL((chain_down_kernel<WT, NW, NTT, KSC, PF>), grid, dim3(KSC * kWave), 0, s, a);
   return hipGetLastError();
 }
 
+// Layers narrower than 4096 take one 16-row half per workgroup: twice the
+// workgroups (two per CU, four waves per SIMD with one token tile) where row
+// pairs leave most CUs idle.  Same-process A/B on the 2048-wide 7B-class
+// layer: 36.7 -> 33.9 us per step at one token, 54.4 -> 49.3 at four; at the
+// 7168-wide DeepSeek-V3 shape single halves were slower (108.3 -> 110.4 us
+// at one token, 525.4 -> 546.7 at 16).
+constexpr int kChainPairMinH = 4096;
+
 template <int WT>
 static hipError_t launch_chain_ntt(const ChainArgs &a, hipStream_t s) {
-  return a.T > kTile ? launch_chain_wt<WT, 2>(a, s) : launch_chain_wt<WT, 1>(a, s);
+  if (a.h < kChainPairMinH)
+    return a.T > kTile ? launch_chain_wt<WT, 1, 2>(a, s) : launch_chain_wt<WT, 1, 1>(a, s);
+  return a.T > kTile ? launch_chain_wt<WT, 2, 2>(a, s) : launch_chain_wt<WT, 2, 1>(a, s);
 }
 
 hipError_t launch_chain(const ChainArgs &a, int wtype, hipStream_t s) {
