@@ -41,7 +41,7 @@ bool has_private(const deamoe_config &c) {
 }
 
 struct Layout {
-  size_t logits, part, topk_ids, topk_w, tok_depts, tok_dept_w, tok_ndept, dept_count,
+  size_t part, topk_ids, topk_w, tok_depts, tok_dept_w, tok_ndept, dept_count,
       dept_offset, dept_tokens, exp_count, exp_offset, exp_tokens;
   size_t counts, units[kMaxStages], slot_pair, slot_w, nslot, tok_exp_pair, exp_src, pair_dept;
   size_t abuf_dept, abuf_exp, abuf_se, gbuf, ubuf, ybuf, zbuf, zsbuf, partial;
@@ -65,7 +65,6 @@ Layout make_layout(const deamoe_config &c) {
     off = align_up(off + (bytes ? bytes : 1));
     return o;
   };
-  L.logits = take(T * n * 4);
   L.part = take((size_t)L.kc * T * 64 * route_ns(c.n_experts) * 4);
   L.topk_ids = take(T * k * 4);
   L.topk_w = take(T * k * 4);
@@ -240,18 +239,21 @@ int down_ks_of(const deamoe_config &c, int T) {
 // up to 32 tokens (two token tiles from 17 on); below kChainMinTiles
 // workgroups (a hidden size under 4096) only up to 4 tokens, where the
 // separate down stage has too few work items to do better (measured on the
-// 2048-wide layer).  FACTORED: up to 16 tokens; its department down stage is
-// a few long contractions that the split-K stage already streams well, and
-// the fused kernel gains only with a grid of at least kChainMinTilesFactored
-// workgroups (measured on the 7168- and 4096-wide Table 1 layers).
-constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 192;
+// 2048-wide layer).  FACTORED: up to 16 tokens at every Table 1 width (at
+// least kChainMinTilesFactored row pairs, h >= 1024): the fused kernel saves
+// the combine launch.  Same-process A/B against the separate department down
+// stage and combine, us per step: Baseline-7B (h = 1024) 38.3 -> 36.3 at one
+// token, 77.7 -> 75.6 at 16; Qwen3 (h = 4096, with 16-row blocks) 79.8 ->
+// 76.9 at one token, 220.7 -> 214.4 at 8, 308.2 -> 305.1 at 16; DeepSeek-V2
+// (h = 5120) 90.3 -> 86.6 at one token, 389.7 -> 389.0 at 16.
+constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 32;
 bool use_chain(const deamoe_config &c, int T) {
   if (T > kChainT) return false;
   // the plan builds the fused kernel's units for one token group only
   if (token_groups_max(c, T) > 1) return false;
   const int tiles = c.hidden / (2 * kTile);
   if (c.form == DEAMOE_FORM_FACTORED && (T > kTile || tiles < kChainMinTilesFactored)) return false;
-  if (T > 4 && tiles < kChainMinTiles) return false;
+  if (c.form == DEAMOE_FORM_SLICE && T > 4 && tiles < kChainMinTiles) return false;
   const int dk = std::min(c.top_k_dept > 0 ? c.top_k_dept : c.top_k, std::min(c.top_k, c.n_depts));
   const bool slice_priv = c.form == DEAMOE_FORM_SLICE && c.d_private > 0;
   const int units = std::min(c.n_depts, T * dk) +
@@ -422,9 +424,8 @@ deamoe_routing routing_in_ws(void *ws, const Layout &L, const deamoe_routing *us
     r.exp_count = at<int32_t>(ws, L.exp_count);
     r.exp_offset = at<int32_t>(ws, L.exp_offset);
     r.exp_tokens = at<int32_t>(ws, L.exp_tokens);
-    r.logits = nullptr;
+    r.logits = nullptr;   // no kernel reads them back
   }
-  if (!r.logits) r.logits = at<float>(ws, L.logits);
   return r;
 }
 

@@ -232,13 +232,15 @@ static hipError_t launch_chain_wt(const ChainArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Layers narrower than 4096 take one 16-row half per workgroup: twice the
+// Layers narrower than 5120 take one 16-row half per workgroup: twice the
 // workgroups (two per CU, four waves per SIMD with one token tile) where row
 // pairs leave most CUs idle.  Same-process A/B on the 2048-wide 7B-class
-// layer: 36.7 -> 33.9 us per step at one token, 54.4 -> 49.3 at four; at the
-// 7168-wide DeepSeek-V3 shape single halves were slower (108.3 -> 110.4 us
-// at one token, 525.4 -> 546.7 at 16).
-constexpr int kChainPairMinH = 4096;
+// layer: 36.7 -> 33.9 us per step at one token, 54.4 -> 49.3 at four; on
+// the 4096-wide Qwen3 FACTORED layer 79.2 -> 76.9 at one token, 312.3 ->
+// 305.1 at 16.  At 5120 (DeepSeek-V2 FACTORED: 86.6 -> 88.1 at one token,
+// 389.0 -> 393.5 at 16) and at the 7168-wide DeepSeek-V3 shape (108.3 ->
+// 110.4 us at one token, 525.4 -> 546.7 at 16) single halves were slower.
+constexpr int kChainPairMinH = 5120;
 
 template <int WT>
 static hipError_t launch_chain_ntt(const ChainArgs &a, hipStream_t s) {

@@ -50,16 +50,6 @@ __device__ inline uint64_t wave_max_u64(uint64_t v) {
   return best;
 }
 
-// Arg-max by (value desc, index asc) over the lanes' candidates; a lane with
-// no candidate passes valid = false.  Returns the winning index (every lane).
-__device__ inline int wave_argmax_idx(float v, int i, bool valid, float &best_v) {
-  const uint64_t key = valid ? (((uint64_t)ord_u32(v) << 32) | (uint32_t)~(uint32_t)i) : 0ull;
-  const uint64_t b = wave_max_u64(key);
-  const uint32_t ob = (uint32_t)(b >> 32);
-  best_v = __uint_as_float((ob & 0x80000000u) ? (ob & 0x7fffffffu) : ~ob);
-  return (int)~(uint32_t)b;
-}
-
 // DPP exchange of a 32-bit value within rows of 16 lanes.
 template <int CTRL>
 __device__ inline float dpp_f32(float v) {
@@ -320,6 +310,7 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
   if (lds.eb && lane < (n + 31) / 32) lds.eb[lane] = 0;
 
   float lv[NS];
+  uint32_t nanbits = 0;   // bit s: expert e0 + s has a NaN logit
   {
     float l[NS];
     if (a.logits_in) {
@@ -353,8 +344,8 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
     }
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      if (gw && e0 + s < n) a.r.logits[(size_t)t * n + e0 + s] = l[s];
       lv[s] = (e0 + s < n && l[s] == l[s]) ? l[s] : -INFINITY;   // NaN ranks last
+      nanbits |= (uint32_t)(l[s] != l[s]) << s;
     }
   }
 
@@ -378,38 +369,58 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
   if (a.kdept > 0) {
     if (lane < m) s_gs[lane] = ord_key(-INFINITY);
     wave_lds_sync();
-    // the lane's run of experts spans few departments: one atomic per
-    // department of the run, with the run's maximum in it
-    int cur = dep[0], best = ord_key(-INFINITY);
+    if (E >= NS) {
+      // the lane's run of experts spans at most two departments, dep[0] and
+      // dep[0] + 1: both maxima in straight-line code, one atomic each
+      int b0 = ord_key(-INFINITY), b1 = b0;
+      bool two = false;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      if (e0 + s >= n) break;
-      if (dep[s] != cur) {
-        atomicMax(&s_gs[cur], best);
-        cur = dep[s];
-        best = ord_key(-INFINITY);
+      for (int s = 0; s < NS; ++s) {
+        const int kv = ord_key(lv[s]);   // -inf past the last expert
+        const bool first = dep[s] == dep[0];
+        b0 = first ? max(b0, kv) : b0;
+        b1 = first ? b1 : max(b1, kv);
+        two |= !first && e0 + s < n;
       }
-      best = max(best, ord_key(lv[s]));
+      if (e0 < n) atomicMax(&s_gs[dep[0]], b0);
+      if (two) atomicMax(&s_gs[dep[0] + 1], b1);
+    } else {
+      // one atomic per department of the run, with the run's maximum in it
+      int cur = dep[0], best = ord_key(-INFINITY);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        if (e0 + s >= n) break;
+        if (dep[s] != cur) {
+          atomicMax(&s_gs[cur], best);
+          cur = dep[s];
+          best = ord_key(-INFINITY);
+        }
+        best = max(best, ord_key(lv[s]));
+      }
+      if (e0 < n) atomicMax(&s_gs[cur], best);
     }
-    if (e0 < n) atomicMax(&s_gs[cur], best);
     wave_lds_sync();
-    const float gsv = lane < m ? ord_val(s_gs[lane]) : -INFINITY;
-    keep = 0;
-    for (int r = 0; r < a.kdept; ++r) {
-      float bv;
-      const int bj = wave_argmax_idx(gsv, lane, lane < m && !((keep >> lane) & 1), bv);
-      keep |= 1ull << (bj & 63);
+    // department j is kept if fewer than kdept departments rank before it
+    // by (score desc, id asc); lane j counts them with one pass over the m
+    // scores (the order keys of -0 and +0 agree, as in the expert keys)
+    const uint32_t gu = lane < m ? ord_u32(ord_val(s_gs[lane])) : 0u;
+    int before = 0;
+    for (int i = 0; i < m; ++i) {
+      const uint32_t gi = __builtin_amdgcn_readlane(gu, i);
+      before += gi > gu || (gi == gu && i < lane);
     }
+    keep = __ballot(lane < m && before < a.kdept);
   }
 
   // order keys; experts that may not be chosen get 0, below every eligible
   // key (the key of -inf is 0x007fffff)
+  // (keep is all ones without a group limit; bitwise operators, not && and
+  // ||, so that no branch splits the wave per expert)
   uint32_t key[NS];
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
-    const int e = e0 + s;
-    const bool ok = e < n && (a.kdept == 0 || ((keep >> (dep[s] & 63)) & 1));
-    key[s] = ok ? ord_u32(lv[s]) : 0u;
+    const uint32_t ok = (uint32_t)(e0 + s < n) & (uint32_t)(keep >> (dep[s] & 63));
+    key[s] = (ok & 1u) ? ord_u32(lv[s]) : 0u;
   }
   // Candidates.  theta, the k-th largest of the per-lane maxima, bounds the
   // k-th largest key from below (k lanes hold a key >= theta), so every
@@ -629,6 +640,15 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
       if (a.d_se > 0) a.slot_w[(size_t)t * S + ns] = 1.0f;
       a.nslot[t] = ns + (a.d_se > 0 ? 1 : 0);
     }
+  }
+  // the logits last: a wave may not reuse the registers of a store's data
+  // until the store completes, so stores issued early would stall the
+  // selection above
+  if (gw && a.r.logits) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      if (e0 + s < n)
+        a.r.logits[(size_t)t * n + e0 + s] = ((nanbits >> s) & 1u) ? __builtin_nanf("") : lv[s];
   }
 }
 

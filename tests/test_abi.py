@@ -280,8 +280,10 @@ def test_trace_points():
     # group-limited routing with long tiles routes inside the first stage
     # only while (nearly) all of its tiles fit in one round (one token here)
     assert [D.deamoe_trace_points(f, T) for T in (1, 2, 4, 5, 16, 17)] == [7, 8, 8, 8, 8, 9]
-    q = D.make_config(W.PRESETS["qwen3_factored"].layer, 64)   # h 4096: separate stages
-    assert [D.deamoe_trace_points(q, T) for T in (1, 16)] == [8, 9]
+    q = D.make_config(W.PRESETS["qwen3_factored"].layer, 64)   # h 4096: fused up to 16 tokens
+    assert [D.deamoe_trace_points(q, T) for T in (1, 16, 17)] == [7, 8, 9]
+    b7 = D.make_config(W.PRESETS["base7b_factored"].layer, 64)   # h 1024: the same
+    assert [D.deamoe_trace_points(b7, T) for T in (1, 16, 17)] == [7, 8, 9]
     k2 = D.make_config(W.PRESETS["kimik2_factored"].layer, 64)   # 1280 experts
     assert D.deamoe_trace_points(k2, 1) == 8
     # more active units than the fused kernel's table holds: separate stages
