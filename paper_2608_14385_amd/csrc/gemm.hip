@@ -32,8 +32,8 @@ __device__ __attribute__((always_inline)) void grouped_gemm_body(const GemmStage
       u = lo;
     }
     u = uniform(u);
-    const GemmUnit *U = st.units + u;
-    Run::run(sm, U, active ? tile - uniform(s_begin[u]) : 0, active, st.sigma);
+    const GemmUnit U = load_unit(st.units + u);
+    Run::run(sm, &U, active ? tile - uniform(s_begin[u]) : 0, active, st.sigma);
   }
 }
 

@@ -71,6 +71,35 @@ __device__ inline bf16x8 fp8x8_to_bf16(uint32_t lo, uint32_t hi) {
   return r;
 }
 
+// Global-address-space view of a pointer.  Pointers read from a unit table
+// or an LDS copy of the arguments leave the compiler without the knowledge
+// that they address global memory: accesses through them would become flat
+// accesses, which also count as LDS operations, so every later LDS wait
+// would wait for them too (a store's full round trip).
+template <class T>
+using gmem = __attribute__((address_space(1))) T;
+template <class T>
+__device__ inline gmem<T> *glob(T *p) {
+  return reinterpret_cast<gmem<T> *>(reinterpret_cast<uintptr_t>(p));
+}
+
+// A unit of a stage table, read once per work item with scalar loads: the
+// table is constant while a stage runs.  The tile loop and the epilogue then
+// take every field from scalar registers; a field read through the table
+// pointer would be a vector load, and a vector load issued after the weight
+// prefetch can only be waited for together with it.
+__device__ inline GemmUnit load_unit(const GemmUnit *p) {
+  const auto *c = reinterpret_cast<const __attribute__((address_space(4))) GemmUnit *>(
+      reinterpret_cast<uintptr_t>(p));
+  GemmUnit u;
+  u.w0 = c->w0; u.w1 = c->w1; u.s0 = c->s0; u.s1 = c->s1;
+  u.in0 = c->in0; u.in1 = c->in1; u.idx = c->idx; u.out0 = c->out0; u.out1 = c->out1;
+  u.R = c->R; u.K = c->K; u.ldw = c->ldw; u.ldin = c->ldin; u.ldout = c->ldout;
+  u.ntok = c->ntok; u.tile_begin = c->tile_begin; u.epi = c->epi; u.out_f32 = c->out_f32;
+  u.tpg = c->tpg;
+  return u;
+}
+
 typedef __attribute__((address_space(1))) const u32x4 gvec;
 typedef __attribute__((address_space(1))) const float gfloat;
 
@@ -82,6 +111,8 @@ __device__ inline const gfloat *gfptr(const float *p) {
 }
 
 // Token-operand row of token i of a unit.
+// idx is a generic pointer: the small-batch kernel keeps its token lists in
+// LDS, the stage tables in global memory.
 __device__ inline const char *token_row(const void *base, const int32_t *idx, int ldin, int i,
                                         int abytes) {
   const int row = idx ? idx[i] : i;
@@ -316,18 +347,18 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
 // false writes only the first `left` of them.
 __device__ inline void store4(void *base, int out_f32, size_t off, f32x4 o, bool full, int left) {
   if (out_f32) {
-    float *p = static_cast<float *>(base) + off;
+    gmem<float> *p = glob(static_cast<float *>(base)) + off;
     if (full) {
-      *reinterpret_cast<f32x4 *>(p) = o;
+      *reinterpret_cast<gmem<f32x4> *>(p) = o;
     } else {
       for (int r = 0; r < left; ++r) p[r] = o[r];
     }
   } else {
-    uint16_t *p = static_cast<uint16_t *>(base) + off;
+    gmem<uint16_t> *p = glob(static_cast<uint16_t *>(base)) + off;
     if (full) {
       const uint32_t lo = f32_to_bf16(o[0]) | ((uint32_t)f32_to_bf16(o[1]) << 16);
       const uint32_t hi = f32_to_bf16(o[2]) | ((uint32_t)f32_to_bf16(o[3]) << 16);
-      *reinterpret_cast<u32x2 *>(p) = u32x2{lo, hi};
+      *reinterpret_cast<gmem<u32x2> *>(p) = u32x2{lo, hi};
     } else {
       for (int r = 0; r < left; ++r) p[r] = f32_to_bf16(o[r]);
     }
@@ -414,7 +445,9 @@ struct TileRunner {
     alignas(16) char buf[4][WAVE_BYTES];   // staging, then (KS > 1) partial tiles
   };
 
-  __device__ static void run(Smem &sm, const GemmUnit *U, int item, bool active, int sigma) {
+  // U: the unit in registers (load_unit for a table entry).
+  __device__ __attribute__((always_inline)) static void run(Smem &sm, const GemmUnit *U, int item,
+                                                            bool active, int sigma) {
     const int wave = uniform(threadIdx.x / kWave), lane = lane_id();
     const int kp = uniform(wave % KS);
     item = uniform(item);

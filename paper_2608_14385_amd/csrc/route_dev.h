@@ -193,17 +193,6 @@ __device__ inline void wave_lds_sync() {
 
 constexpr int kMaxKC = 16;   // router chunks (host caps the split)
 
-// Global-address-space view of a pointer.  The plan reads its pointers from
-// an LDS copy of the argument block, which leaves the compiler without the
-// knowledge that they address global memory (stores through them would
-// become flat stores, which also hold up every later LDS wait).
-template <class T>
-using gmem = __attribute__((address_space(1))) T;
-template <class T>
-__device__ inline gmem<T> *glob(T *p) {
-  return reinterpret_cast<gmem<T> *>(reinterpret_cast<uintptr_t>(p));
-}
-
 // Fill one unit of a stage table field by field (no temporary struct).
 __device__ inline void put_unit(gmem<GemmUnit> *U, const void *w0, const void *w1, const float *s0,
                                 const float *s1, const void *in0, const void *in1,
@@ -298,8 +287,11 @@ struct PlanIn {
 // gw: write the routing results to global memory (false: LDS outputs only,
 // for workgroups that need the routing but do not publish it).
 template <int NS>
-__device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSmem &sm,
-                          PlanIn lds = {nullptr, nullptr, nullptr, nullptr}, const bool gw = true) {
+__device__ __attribute__((always_inline)) void route_one(const RouteArgs &a, const int t,
+                                                        const int lane, TokSmem &sm,
+                                                        PlanIn lds = {nullptr, nullptr, nullptr,
+                                                                      nullptr},
+                                                        const bool gw = true) {
   uint64_t *s_sel = sm.sel, *s_ord = sm.ord;
   int32_t *s_gs = sm.gs;
   uint32_t *s_db = sm.db;
@@ -386,16 +378,18 @@ __device__ void route_one(const RouteArgs &a, const int t, const int lane, TokSm
       if (two) atomicMax(&s_gs[dep[0] + 1], b1);
     } else {
       // one atomic per department of the run, with the run's maximum in it
+      // (predicated, not an early exit, so that the loop unrolls and dep
+      // stays in registers)
       int cur = dep[0], best = ord_key(-INFINITY);
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        if (e0 + s >= n) break;
-        if (dep[s] != cur) {
+        const bool in = e0 + s < n;
+        if (in && dep[s] != cur) {
           atomicMax(&s_gs[cur], best);
           cur = dep[s];
           best = ord_key(-INFINITY);
         }
-        best = max(best, ord_key(lv[s]));
+        best = in ? max(best, ord_key(lv[s])) : best;
       }
       if (e0 < n) atomicMax(&s_gs[cur], best);
     }
