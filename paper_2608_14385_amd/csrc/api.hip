@@ -183,16 +183,16 @@ int token_groups_max(const deamoe_config &c, int T) {
   const int gt = kTile * wave_ntt_of(c, T);
   return (T + gt - 1) / gt;
 }
-// Token tiles per wave in the separate down stages.  The SLICE down stage
-// keeps one tile up to 64 tokens: its row-pair tiles then fit three waves
-// per SIMD (two with two tiles), which outweighs streaming the rows of a
-// unit with more than 16 tokens once per group (same-process A/B, us per
-// step, two tiles -> one: DeepSeek-V3 shape 764.7 -> 748.3 at 48 tokens,
-// 827.2 -> 824.1 at 64; fp8 505.7 -> 494.5 and the 7B-class layer 119.6 ->
-// 112.9 at 64).  With 128 tokens routing is usually skewed enough that the
-// extra passes cost more (the skewed preset 510.1 -> 520.4).
+// Token tiles per wave in the separate down stages (above 32 tokens for
+// SLICE).  Layers narrower than 4096 keep one tile up to 64 tokens: there
+// the one-tile row pairs at three waves per SIMD outweigh streaming the rows
+// of a unit with more than 16 tokens once per group (same-process A/B, us
+// per step, one tile -> two: the 7B-class layer 89.4 -> 104.3 at 48 tokens,
+// 106.2 -> 110.5 at 64).  Wider layers take two (the DeepSeek-V3 shape
+// 776.5 -> 775.3 at 56, 819.6 -> 806.3 at 64; fp8 482.7 -> 480.4 and skewed
+// routing 368.5 -> 361.5 at 64; even at 48).
 int down_ntt_of(const deamoe_config &c, int T) {
-  return c.form == DEAMOE_FORM_SLICE && T <= 64 ? 1 : wave_ntt_of(c, T);
+  return c.form == DEAMOE_FORM_SLICE && T <= 64 && c.hidden < 4096 ? 1 : wave_ntt_of(c, T);
 }
 int down_groups_max(const deamoe_config &c, int T) {
   const int gt = kTile * down_ntt_of(c, T);
