@@ -39,9 +39,9 @@ HBM_PEAK_GBPS = 8000.0
 #  - the average launch duration from a kernel-trace run of the default
 #    command (profiles/gate_up_dsv3_bf16_T16_kernel_trace.md), which excludes
 #    the launch gap that the benchmark's own events include.
-TRAFFIC_BYTES = 2341135360
-PROFILED_GATE_UP_US = 352.43
-TRAFFIC_SOURCES_SHA256 = "57de8d8576800f462023dde6ceddcb5ae4cf487e48b015711fd43d43e254eee5"
+TRAFFIC_BYTES = 2341119795
+PROFILED_GATE_UP_US = 338.97
+TRAFFIC_SOURCES_SHA256 = "a5331629f43cc0bb8e7fd5ad0e457cf9f0c4ce1cf4127457483d7919c8a1358f"
 
 
 def library_sources_digest() -> str:
