@@ -224,10 +224,16 @@ constexpr int kDownRows = 2 * kTile;
 // over two waves up to two tokens, where the batch leaves few work items);
 // the FACTORED form (every contraction d long) splits K four ways up to 8
 // tokens and two ways up to 32 (64 where h >= 4096), while the batch leaves
-// too few tiles to occupy the waves.
+// too few tiles to occupy the waves.  From 9 to 16 tokens the split follows
+// the contraction: four ways for d >= 2048, none for d < 1024 (same-process
+// A/B at 16 tokens, us per step: the DeepSeek-V3 FACTORED layer 711.2 ->
+// 698.6, Kimi-K2 852.2 -> 846.2, Baseline-7B 71.5 -> 70.2; Qwen3 and
+// DeepSeek-V2, d = 1536, were even either way).
 int down_ks_of(const deamoe_config &c, int T) {
   if (c.form == DEAMOE_FORM_SLICE) return T <= 2 ? 2 : 1;
   if (T <= 8) return 4;
+  if (T <= 16 && c.d_shared >= 2048) return 4;
+  if (T <= 16 && c.d_shared < 1024) return 1;
   const bool wide = c.hidden >= 4096;
   return T <= 32 || (wide && T <= 64) ? 2 : 1;
 }
