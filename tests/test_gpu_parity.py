@@ -53,11 +53,19 @@ def test_tiny_f32_slice(T):
                                      "sigmoid", "sigmoid_no_renorm_scaled", "group_limited",
                                      "shared_expert", "no_private", "t3_group_limited",
                                      "t2_shared_expert", "t4_zipf_sigmoid_scaled",
-                                     "t1_strict_cover", "t3_fp8"])
+                                     "t1_strict_cover", "t3_fp8", "narrow_depts",
+                                     "t2_narrow_depts"])
 def test_small_variants(variant):
     """Gate and layer variants on a small layer; the t<N> cases are batches
-    of at most four tokens, which route inside the gate/up launch."""
+    of at most four tokens, which route inside the gate/up launch.  The
+    narrow_depts cases have departments of 5 experts under a group limit, fewer
+    than the 8 logits each routing lane holds, so a lane's run spans up to
+    three departments."""
     T = 9
+    if variant in ("narrow_depts", "t2_narrow_depts"):
+        cfg = small(n_experts=320, n_depts=64, top_k=8, top_k_dept=4)
+        check_case(Case(cfg, 2 if variant == "t2_narrow_depts" else T, seed=16))
+        return
     if variant == "t3_group_limited":
         check_case(Case(small(n_experts=64, n_depts=8, top_k=6, top_k_dept=3), 3, seed=11))
         return
