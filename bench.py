@@ -39,9 +39,9 @@ HBM_PEAK_GBPS = 8000.0
 #  - the average launch duration from a kernel-trace run of the default
 #    command (profiles/gate_up_dsv3_bf16_T16_kernel_trace.md), which excludes
 #    the launch gap that the benchmark's own events include.
-TRAFFIC_BYTES = 2341119795
-PROFILED_GATE_UP_US = 338.97
-TRAFFIC_SOURCES_SHA256 = "a5331629f43cc0bb8e7fd5ad0e457cf9f0c4ce1cf4127457483d7919c8a1358f"
+TRAFFIC_BYTES = 2341120000
+PROFILED_GATE_UP_US = 338.04
+TRAFFIC_SOURCES_SHA256 = "40f066df0054b7461a05da71f25852331d1d1e48f65915c7b8506a226b355142"
 
 
 def library_sources_digest() -> str:
