@@ -75,14 +75,18 @@ __global__ __launch_bounds__(BT) void plan_kernel(RouteArgs a) {
   plan_body<BT>(sa, sm);
 }
 
-// Batches of at most kFusedMaxT tokens route and plan in one workgroup: wave
-// t routes token t (one routing wave per SIMD) and leaves its results in LDS
-// as well, and the plan starts after a barrier that waits for LDS only (the
-// results' global stores complete in the background).  Larger batches route
-// in a workgroup per token, which spreads the routing over as many CUs.
-// Wider routers (more experts per lane) take fewer waves for the plan, which
-// leaves each wave more registers.
-constexpr int kFusedMaxT = 4;
+// Batches of at most kFusedMaxT tokens (and no more than the workgroup has
+// waves) route and plan in one workgroup: wave t routes token t and leaves
+// its results in LDS as well, and the plan starts after a barrier that waits
+// for LDS only (the results' global stores complete in the background).
+// Larger batches route in a workgroup per token, which spreads the routing
+// over as many CUs.  Wider routers (more experts per lane) take fewer waves
+// for the plan, which leaves each wave more registers.  Same-process A/B of
+// one workgroup against the two kernels, us per step: the DeepSeek-V3 shape
+// 358.4 -> 357.0 at 6 tokens and 410.9 -> 409.8 at 8; fp8 182.1 -> 180.7 at
+// 5; the 7B-class layer 72.2 -> 70.9 and Qwen3 209.6 -> 208.4 at 8; routers
+// of 16 experts per lane even.
+constexpr int kFusedMaxT = 8;
 template <int NS>
 constexpr int fused_waves() { return NS <= 4 ? 16 : NS <= 16 ? 8 : 4; }
 
@@ -100,7 +104,7 @@ __global__ __launch_bounds__(fused_waves<NS>() * 64) void route_plan_kernel(Rout
 
 template <int NS>
 static hipError_t launch_route_ns(const RouteArgs &a, hipStream_t s) {
-  if (a.T <= kFusedMaxT) {
+  if (a.T <= kFusedMaxT && a.T <= fused_waves<NS>()) {
     hipLaunchKernelGGL((route_plan_kernel<NS>), dim3(1), dim3(fused_waves<NS>() * 64), 0, s, a);
     return hipGetLastError();
   }
