@@ -242,24 +242,26 @@ int down_ks_of(const deamoe_config &c, int T) {
 // Down projections and combine fused into one kernel (the SLICE down stage,
 // the FACTORED department down stage): batches whose active units fit the
 // kernel's unit table.  Its grid is one workgroup per 32 rows of y.  SLICE:
-// up to 32 tokens (two token tiles from 17 on); below kChainMinTiles
-// workgroups (a hidden size under 4096) only up to 4 tokens, where the
-// separate down stage has too few work items to do better (measured on the
-// 2048-wide layer).  FACTORED: up to 16 tokens at every Table 1 width (at
+// up to 32 tokens (two token tiles from 17 on); below kChainMinTiles row
+// pairs (a hidden size under 4096, where the kernel takes 16-row blocks) up
+// to kChainNarrowMaxT tokens (same-process A/B on the 2048-wide 7B-class
+// layer against the separate down stage and combine, us per step: 66.5 ->
+// 61.5 at 5 tokens, 81.0 -> 76.1 at 16, 89.6 -> 85.6 at 24, but 89.9 ->
+// 91.1 at 32).  FACTORED: up to 16 tokens at every Table 1 width (at
 // least kChainMinTilesFactored row pairs, h >= 1024): the fused kernel saves
 // the combine launch.  Same-process A/B against the separate department down
 // stage and combine, us per step: Baseline-7B (h = 1024) 38.3 -> 36.3 at one
 // token, 77.7 -> 75.6 at 16; Qwen3 (h = 4096, with 16-row blocks) 79.8 ->
 // 76.9 at one token, 220.7 -> 214.4 at 8, 308.2 -> 305.1 at 16; DeepSeek-V2
 // (h = 5120) 90.3 -> 86.6 at one token, 389.7 -> 389.0 at 16.
-constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 32;
+constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 32, kChainNarrowMaxT = 24;
 bool use_chain(const deamoe_config &c, int T) {
   if (T > kChainT) return false;
   // the plan builds the fused kernel's units for one token group only
   if (token_groups_max(c, T) > 1) return false;
   const int tiles = c.hidden / (2 * kTile);
   if (c.form == DEAMOE_FORM_FACTORED && (T > kTile || tiles < kChainMinTilesFactored)) return false;
-  if (c.form == DEAMOE_FORM_SLICE && T > 4 && tiles < kChainMinTiles) return false;
+  if (c.form == DEAMOE_FORM_SLICE && T > kChainNarrowMaxT && tiles < kChainMinTiles) return false;
   const int dk = std::min(c.top_k_dept > 0 ? c.top_k_dept : c.top_k, std::min(c.top_k, c.n_depts));
   const bool slice_priv = c.form == DEAMOE_FORM_SLICE && c.d_private > 0;
   const int units = std::min(c.n_depts, T * dk) +

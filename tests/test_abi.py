@@ -272,8 +272,8 @@ def test_trace_points():
     c = cfg_c3()
     assert [D.deamoe_trace_points(c, T) for T in (1, 4, 5, 16, 17, 32, 33, 64)] == \
         [4, 4, 5, 5, 5, 5, 6, 6]
-    s7 = D.make_config(W.PRESETS["7b_bf16"].layer, 64)     # h 2048: fused up to 4 tokens
-    assert [D.deamoe_trace_points(s7, T) for T in (1, 4, 5, 16)] == [4, 4, 6, 6]
+    s7 = D.make_config(W.PRESETS["7b_bf16"].layer, 64)     # h 2048: fused up to 24 tokens
+    assert [D.deamoe_trace_points(s7, T) for T in (1, 4, 5, 16, 24, 25)] == [4, 4, 5, 5, 5, 6]
     # routers of more than 1024 experts keep the separate routing kernel
     assert D.deamoe_trace_points(cfg_c3(n_experts=2048, n_depts=32), 1) == 5
     f = D.make_config(W.PRESETS["dsv3_factored"].layer, 64)

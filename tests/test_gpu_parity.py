@@ -202,7 +202,7 @@ def test_tiny_baseline(T):
     check_case(Case(cfg, T, seed=30 + T), baseline=True)
 
 
-@pytest.mark.parametrize("T", [1, 4, 16])
+@pytest.mark.parametrize("T", [1, 4, 16, 24, 32])
 def test_7b_bf16(T):
     check_case(Case(P["7b_bf16"].layer, T, seed=40 + T, logits="uniform"))
 
