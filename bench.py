@@ -40,8 +40,8 @@ HBM_PEAK_GBPS = 8000.0
 #    command (profiles/gate_up_dsv3_bf16_T16_kernel_trace.md), which excludes
 #    the launch gap that the benchmark's own events include.
 TRAFFIC_BYTES = 2341120000
-PROFILED_GATE_UP_US = 338.04
-TRAFFIC_SOURCES_SHA256 = "40f066df0054b7461a05da71f25852331d1d1e48f65915c7b8506a226b355142"
+PROFILED_GATE_UP_US = 337.01
+TRAFFIC_SOURCES_SHA256 = "348bd1b66b144cc86aeb5f7a4fa5dcda14a6b0ce6208a8a86fba1b95b47ca4d6"
 
 
 def library_sources_digest() -> str:
