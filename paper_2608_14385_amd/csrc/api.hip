@@ -169,15 +169,22 @@ int validate_weights(const deamoe_config &c, const deamoe_weights *w, bool need_
 
 int ntt_of(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
 
-// Token tiles per wave in the expert stages: at most 2, so that row pairs
-// and two-matrix tiles keep their accumulators in registers.  A unit with
-// more tokens than one wave holds gets one work item per token group.  The
-// FACTORED stages keep one tile at every batch: its private gate/up then
-// runs at three waves per SIMD, which outweighs streaming the rows of a
-// unit with more than 16 tokens once per group.
+// Token tiles per wave in the gate/up stage.  A unit with more tokens than
+// one wave holds gets one work item per token group, and every group
+// streams the unit's rows.  SLICE: one tile up to 16 tokens, two above, and
+// four above 96 tokens on layers at least 4096 wide.  Same-process A/B, us
+// per step, two tiles -> four, outputs bit-identical: the DeepSeek-V3 shape
+// 1005.7 -> 973.9 at 128 tokens (900.0 -> 897.3 at 96), fp8 651.7 -> 635.8
+// at 128 (563.9 -> 569.1 at 96), skewed routing 500.9 -> 499.4 at 128
+// (436.3 -> 439.5 at 96); the 2048-wide 7B-class layer 145.8 -> 153.1 at
+// 128, where four tiles halve its work items and leave the three-wave
+// two-tile kernel for a two-wave one.  The FACTORED stages keep one tile at
+// every batch: its private gate/up then runs at three waves per SIMD, which
+// outweighs streaming the rows of a unit with more than 16 tokens once per
+// group.
 int wave_ntt_of(const deamoe_config &c, int T) {
   if (c.form == DEAMOE_FORM_FACTORED) return 1;
-  return T <= kTile ? 1 : 2;
+  return T <= kTile ? 1 : T <= 96 || c.hidden < 4096 ? 2 : 4;
 }
 int token_groups_max(const deamoe_config &c, int T) {
   const int gt = kTile * wave_ntt_of(c, T);
@@ -191,8 +198,10 @@ int token_groups_max(const deamoe_config &c, int T) {
 // 106.2 -> 110.5 at 64).  Wider layers take two (the DeepSeek-V3 shape
 // 776.5 -> 775.3 at 56, 819.6 -> 806.3 at 64; fp8 482.7 -> 480.4 and skewed
 // routing 368.5 -> 361.5 at 64; even at 48).
+// Row pairs hold at most two token tiles.
 int down_ntt_of(const deamoe_config &c, int T) {
-  return c.form == DEAMOE_FORM_SLICE && T <= 64 && c.hidden < 4096 ? 1 : wave_ntt_of(c, T);
+  return c.form == DEAMOE_FORM_SLICE && T <= 64 && c.hidden < 4096 ? 1
+                                                                     : std::min(2, wave_ntt_of(c, T));
 }
 int down_groups_max(const deamoe_config &c, int T) {
   const int gt = kTile * down_ntt_of(c, T);

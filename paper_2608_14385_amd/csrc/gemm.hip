@@ -65,6 +65,16 @@ void grouped_gemm_occ3_kernel(GemmStage st) {
   grouped_gemm_body<WT, NW, NTT, KS, SPLIT, PAIR, B1>(st);
 }
 
+// Four token tiles per wave (64 tokens), for the gate/up stage of wide
+// layers above 96 tokens: a unit with many tokens streams its rows once per
+// 64 tokens instead of once per 32.  The token operand is requested per step (B1);
+// two waves per SIMD.
+template <int WT, int NW, int NTT, int KS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+void grouped_gemm_wide_kernel(GemmStage st) {
+  grouped_gemm_body<WT, NW, NTT, KS, false, false, true>(st);
+}
+
 // mode: GemmMode; row pairs exist for NTT <= 2 only (the host picks them so).
 // narrow: two-token-tile gate/up pairs run at three waves per SIMD.
 template <int WT, int NW, int NTT, int KS>
@@ -78,6 +88,10 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
     hipLaunchKernelGGL(k, dim3(grid), dim3(256), 0, s, st);
     return hipGetLastError();
   };
+  if constexpr (NTT == 4) {   // four tiles: two-matrix gate/up tiles only
+    if (mode != GEMM_PLAIN) return hipErrorInvalidValue;
+    return plain(grouped_gemm_wide_kernel<WT, NW, NTT, KS>);
+  }
   if constexpr (NW == 2) {
     if (mode == GEMM_SPLIT) {
       if constexpr (NTT == 1)
@@ -102,13 +116,17 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
   return plain(grouped_gemm_kernel<WT, NW, NTT, KS, false, false>);
 }
 
-// Token tiles per wave: 1 or 2 (larger token sets are split into groups).
+// Token tiles per wave: 1, 2, or 4 with a K split over 2 waves (larger
+// token sets are split into groups).
 template <int WT, int NW, int KS>
 static hipError_t dispatch_ntt(const GemmStage &st, int mode, int ntt, int max_tiles, int cap,
                                bool narrow, hipStream_t s) {
   switch (ntt) {
     case 1: return launch_gemm<WT, NW, 1, KS>(st, mode, max_tiles, cap, narrow, s);
     case 2: return launch_gemm<WT, NW, 2, KS>(st, mode, max_tiles, cap, narrow, s);
+    case 4:
+      if constexpr (KS == 2) return launch_gemm<WT, NW, 4, KS>(st, mode, max_tiles, cap, narrow, s);
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }

@@ -202,8 +202,10 @@ def test_tiny_baseline(T):
     check_case(Case(cfg, T, seed=30 + T), baseline=True)
 
 
-@pytest.mark.parametrize("T", [1, 4, 16, 24, 32])
+@pytest.mark.parametrize("T", [1, 4, 16, 24, 32, 100])
 def test_7b_bf16(T):
+    """100 tokens: a layer narrower than 4096 (two token tiles per gate/up
+    wave) with every department in several token groups."""
     check_case(Case(P["7b_bf16"].layer, T, seed=40 + T, logits="uniform"))
 
 
@@ -246,11 +248,13 @@ def test_dsv3_skew_gumbel():
                        max_tokens=128))
 
 
-@pytest.mark.parametrize("T", [1, 2, 4, 8, 16, 32, 64])
+@pytest.mark.parametrize("T", [1, 2, 4, 8, 16, 32, 64, 128])
 def test_dsv3_fp8(T):
     """64 tokens: the gate/up stage with two token tiles and a two-wave K
-    split, the separate down stage and the combine."""
-    check_case(WC.case(P["dsv3_fp8"].layer, T, seed=70 + T, weight_seed=70))
+    split, the separate down stage and the combine; 128: four token tiles
+    per gate/up wave."""
+    check_case(WC.case(P["dsv3_fp8"].layer, T, seed=70 + T, weight_seed=70,
+                       max_tokens=128 if T > 64 else None))
 
 
 @pytest.mark.parametrize("T", [1, 16, 64])
