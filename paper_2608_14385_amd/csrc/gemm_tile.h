@@ -255,6 +255,42 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
     bp0[tt] = token_row(U.in0, U.idx, U.ldin, i, Tr::A_BYTES);
     bp1[tt] = SPLIT ? token_row(U.in1, U.idx, U.ldin, i, Tr::A_BYTES) : bp0[tt];
   }
+  // ROWS: the token operand of two or more tiles is loaded like the weights,
+  // as whole 256-byte row segments (instruction q of tile tt covers tokens
+  // 4q + lane / 16, 16 bytes each), and transposed through this wave's LDS
+  // region one tile at a time.  That touches half the cache lines per load
+  // instruction of the operand layout's 16 rows x 64 bytes.
+  constexpr bool ROWS = WT == WT_BF16 && !SPLIT && NTT >= 2;
+  using LB = WLoad<WT_BF16>;   // token rows are bf16
+  static_assert(!ROWS || (ASEG == LB::WSEG && LB::NQ == 4 && NW * LD::REGION >= LB::REGION),
+                "a token tile is staged like one bf16 weight tile");
+  uint32_t boffs[ROWS ? NTT : 1][4];   // byte offsets from in0 of the rows this lane loads
+  if constexpr (ROWS) {
+#pragma unroll
+    for (int tt = 0; tt < NTT; ++tt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        int i = tt * kTile + q * LB::RPI + lane / LB::LPR;
+        i = tok0 + (i < ntok ? i : 0);
+        boffs[tt][q] = (uint32_t)(token_row(U.in0, U.idx, U.ldin, i, Tr::A_BYTES) -
+                                  static_cast<const char *>(U.in0)) +
+                       (lane % LB::LPR) * 16;
+      }
+  }
+  // the token operand of K step kstep in the load layout (ROWS) or the operand layout
+  auto load_tok = [&](u32x4(&Bb)[NTT][BV], int kstep) {
+    if constexpr (ROWS) {
+      const char *base = static_cast<const char *>(U.in0) + (size_t)kstep * ASEG;
+#pragma unroll
+      for (int tt = 0; tt < NTT; ++tt) {
+        if (tt > 0 && tt >= ntt) break;   // ntt >= 1
+#pragma unroll
+        for (int q = 0; q < 4; ++q) Bb[tt][q] = *gptr(base + boffs[tt][q]);
+      }
+    } else {
+      load_b<WT, NTT, SPLIT>(Bb, bp0, bp1, ntt, (size_t)kstep * ASEG, g);
+    }
+  };
   // load pattern: instruction q covers rows q * RPI + lane / LPR, 16 bytes each
   const int lrow = lane / LD::LPR, lchunk = lane % LD::LPR;
   const char *w0 = static_cast<const char *>(U.w0) + lchunk * 16;
@@ -301,7 +337,7 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
         Gb[n][q] = NT ? __builtin_nontemporal_load(gptr(ok ? (n ? w1 : w0) + woff : dummy))
                       : *gptr(ok ? (n ? w1 : w0) + woff : dummy);
     }
-    if constexpr (!B1) load_b<WT, NTT, SPLIT>(Bb, bp0, bp1, ntt, (size_t)kstep * ASEG, g);
+    if constexpr (!B1) load_tok(Bb, kstep);
     if constexpr (WT == WT_FP8)   // a row pair lies in one scale row
       sc = uniform((((rt0 + sub) * TR) / 128 - srow0) * sblocks + kstep);
   };
@@ -315,13 +351,22 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
     for (int q = 0; q < NB; ++q) {
       const int qn = (q + NB - 1) % NB;   // the buffer consumed one step ago
       if constexpr (B1) {
-        load_b<WT, NTT, SPLIT>(B[0], bp0, bp1, ntt, (size_t)kstep_of(v) * ASEG, g);
+        load_tok(B[0], kstep_of(v));
         __builtin_amdgcn_sched_barrier(0);
       }
       issue(G[qn], B[B1 ? 0 : qn], SC[qn], v + PF);
       __builtin_amdgcn_sched_barrier(0);
       u32x4 a[NW][4];
       stage(G[q], a);
+      if constexpr (ROWS) {   // after the weights' reads, in the same region
+        u32x4(&Bq)[NTT][BV] = B[B1 ? 0 : q];
+#pragma unroll
+        for (int tt = 0; tt < NTT; ++tt) {
+          if (tt > 0 && tt >= ntt) break;
+          stage_weights<WT_BF16, 1>(lds, reinterpret_cast<const u32x4(&)[1][4]>(Bq[tt]),
+                                    reinterpret_cast<u32x4(&)[1][4]>(Bq[tt]));
+        }
+      }
       float sc[NW];
       if constexpr (WT == WT_FP8) {
 #pragma unroll
