@@ -52,7 +52,12 @@ __global__ __launch_bounds__(256) void grouped_gemm_kernel(GemmStage st) {
 //    at 16 tokens on the DeepSeek-V3 FACTORED layer (the stage 405.0 ->
 //    364.3), 2071.8 -> 1977.4 at 64, 148.4 -> 145.3 at one token; Kimi-K2
 //    879.6 -> 839.6, DeepSeek-V2 406.2 -> 391.6, Qwen3 330.8 -> 319.5 at 16;
-//  - fp8 stages with two token tiles;
+//  - fp8 stages with two token tiles: with the token operand requested per
+//    step (B1) and loaded as whole row segments for row pairs and for gate/up
+//    pairs with a K split over 2 waves (above 32 tokens; same-process A/B at
+//    the DeepSeek-V3 shape, us per step: 477.6 -> 458.4 at 64 tokens, 631.0
+//    -> 569.1 at 128), double-buffered at 17-32 tokens (348.5 -> 351.4 at 24
+//    with B1);
 //  - bf16 and fp32 stages with two token tiles whose token operand is
 //    requested per step (B1): row pairs (same-process A/B at the DeepSeek-V3
 //    shape, down stage at 128 tokens 378.3 -> 370.0 us, skewed 178.9 ->
@@ -101,14 +106,14 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
     }
     if (mode == GEMM_PAIR) {
       if constexpr (NTT == 2)
-        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, true, !FP8>);
+        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, true, true>);
       else if constexpr (NTT == 1)
         return plain(grouped_gemm_kernel<WT, NW, NTT, KS, false, true>);
       return hipErrorInvalidValue;   // row pairs are built for up to two token tiles
     }
     if constexpr (NTT == 2 && KS > 1) {
       if constexpr (FP8)
-        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, false, false>);
+        return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, false, KS == 2>);
       else if (narrow)
         return plain(grouped_gemm_occ3_kernel<WT, NW, NTT, KS, false, false, true>);
     }

@@ -259,8 +259,10 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
   // as whole 256-byte row segments (instruction q of tile tt covers tokens
   // 4q + lane / 16, 16 bytes each), and transposed through this wave's LDS
   // region one tile at a time.  That touches half the cache lines per load
-  // instruction of the operand layout's 16 rows x 64 bytes.
-  constexpr bool ROWS = WT == WT_BF16 && !SPLIT && NTT >= 2;
+  // instruction of the operand layout's 16 rows x 64 bytes.  fp8 stages take
+  // it with the operand requested per step (B1): their double-buffered
+  // three-wave instantiations would spill the row offsets.
+  constexpr bool ROWS = (WT == WT_BF16 || (WT == WT_FP8 && B1)) && !SPLIT && NTT >= 2;
   using LB = WLoad<WT_BF16>;   // token rows are bf16
   static_assert(!ROWS || (ASEG == LB::WSEG && LB::NQ == 4 && NW * LD::REGION >= LB::REGION),
                 "a token tile is staged like one bf16 weight tile");
