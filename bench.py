@@ -39,9 +39,9 @@ HBM_PEAK_GBPS = 8000.0
 #  - the average launch duration from a kernel-trace run of the default
 #    command (profiles/gate_up_dsv3_bf16_T16_kernel_trace.md), which excludes
 #    the launch gap that the benchmark's own events include.
-TRAFFIC_BYTES = 2341120000
-PROFILED_GATE_UP_US = 337.01
-TRAFFIC_SOURCES_SHA256 = "348bd1b66b144cc86aeb5f7a4fa5dcda14a6b0ce6208a8a86fba1b95b47ca4d6"
+TRAFFIC_BYTES = 2341137203
+PROFILED_GATE_UP_US = 338.37
+TRAFFIC_SOURCES_SHA256 = "50158d1c5df2e7d76276c47d16dc640cb1b8bbd8e6bc823267e07c5ef472eb8d"
 
 
 def library_sources_digest() -> str:
