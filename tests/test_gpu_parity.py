@@ -150,6 +150,20 @@ def test_fused_down_combine(variant):
     check_case(case, baseline=baseline)
 
 
+@pytest.mark.parametrize("variant", ["f32_t128_se", "bf16_t128_se"])
+def test_four_token_tiles(variant):
+    """Above 96 tokens on layers at least 4096 wide the gate/up stage holds
+    four token tiles per wave: 128 tokens, top-4 over 4 departments, so each
+    department has 84-104 tokens in two token groups of 64 (the second one
+    ragged) and the shared expert two full ones; fp32 weights (the operand
+    layout) and bf16 (whole-segment token rows, a shared expert of 256: bf16
+    widths are multiples of the 128-column K step); every output checked."""
+    base = small(hidden=4096, top_k=4, d_shared_expert=192)
+    if variant == "bf16_t128_se":
+        base = base.replace(w_dtype="bf16", act_dtype="bf16", d_private=128, d_shared_expert=256)
+    check_case(Case(base, 128, seed=52 if variant.startswith("f32") else 53))
+
+
 @pytest.mark.parametrize("T", [1, 4, 19])
 def test_tiny_factored(T):
     check_case(Case(P["tiny_factored"].layer, T, seed=10 + T))
