@@ -198,8 +198,16 @@ int token_groups_max(const deamoe_config &c, int T) {
 // 106.2 -> 110.5 at 64).  Wider layers take two (the DeepSeek-V3 shape
 // 776.5 -> 775.3 at 56, 819.6 -> 806.3 at 64; fp8 482.7 -> 480.4 and skewed
 // routing 368.5 -> 361.5 at 64; even at 48).
-// Row pairs hold at most two token tiles.
+// Row pairs hold at most two token tiles.  The FACTORED down stages (the
+// private B_e and the department W_d^T) take two from 17 tokens on layers at
+// least 4096 wide, where a department's W_d^T then streams once per 32
+// tokens instead of once per 16 (same-process A/B, us per step, outputs
+// bit-identical: DeepSeek-V3 FACTORED 1215.6 -> 1203.9 at 32 tokens and
+// 1960.9 -> 1944.5 at 64, the W_d^T stage 85.2 -> 66.0; Qwen3 494.0 ->
+// 485.7 at 32 and 706.0 -> 695.9 at 64; Kimi-K2 2265.0 -> 2244.4 at 64);
+// the 1024-wide Baseline-7B layer was slower (120.6 -> 124.3 at 64).
 int down_ntt_of(const deamoe_config &c, int T) {
+  if (c.form == DEAMOE_FORM_FACTORED) return T > kTile && c.hidden >= 4096 ? 2 : 1;
   return c.form == DEAMOE_FORM_SLICE && T <= 64 && c.hidden < 4096 ? 1
                                                                      : std::min(2, wave_ntt_of(c, T));
 }
@@ -253,24 +261,30 @@ int down_ks_of(const deamoe_config &c, int T) {
 // kernel's unit table.  Its grid is one workgroup per 32 rows of y.  SLICE:
 // up to 32 tokens (two token tiles from 17 on); below kChainMinTiles row
 // pairs (a hidden size under 4096, where the kernel takes 16-row blocks) up
-// to kChainNarrowMaxT tokens (same-process A/B on the 2048-wide 7B-class
-// layer against the separate down stage and combine, us per step: 66.5 ->
-// 61.5 at 5 tokens, 81.0 -> 76.1 at 16, 89.6 -> 85.6 at 24, but 89.9 ->
-// 91.1 at 32).  FACTORED: up to 16 tokens at every Table 1 width (at
+// to kChainNarrowMaxT tokens from kChainNarrowMinTiles row pairs on
+// (same-process A/B on the 2048-wide 7B-class layer against the separate
+// down stage and combine, us per step: 66.5 -> 61.5 at 5 tokens, 81.0 ->
+// 76.1 at 16, 89.6 -> 85.6 at 24, but 89.9 -> 91.1 at 32), and up to 4
+// tokens on narrower layers, where the kernel's workgroups leave most CUs
+// idle (the 1024-wide Baseline-7B vanilla layer, separate stage against the
+// fused kernel: 58.9 -> 46.5 at 8 tokens, 88.6 -> 64.5 at 16).  FACTORED: up to 16 tokens at every Table 1 width (at
 // least kChainMinTilesFactored row pairs, h >= 1024): the fused kernel saves
 // the combine launch.  Same-process A/B against the separate department down
 // stage and combine, us per step: Baseline-7B (h = 1024) 38.3 -> 36.3 at one
 // token, 77.7 -> 75.6 at 16; Qwen3 (h = 4096, with 16-row blocks) 79.8 ->
 // 76.9 at one token, 220.7 -> 214.4 at 8, 308.2 -> 305.1 at 16; DeepSeek-V2
 // (h = 5120) 90.3 -> 86.6 at one token, 389.7 -> 389.0 at 16.
-constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 32, kChainNarrowMaxT = 24;
+constexpr int kChainMinTiles = 128, kChainMinTilesFactored = 32;
+constexpr int kChainNarrowMinTiles = 64, kChainNarrowMaxT = 24;
 bool use_chain(const deamoe_config &c, int T) {
   if (T > kChainT) return false;
   // the plan builds the fused kernel's units for one token group only
   if (token_groups_max(c, T) > 1) return false;
   const int tiles = c.hidden / (2 * kTile);
   if (c.form == DEAMOE_FORM_FACTORED && (T > kTile || tiles < kChainMinTilesFactored)) return false;
-  if (c.form == DEAMOE_FORM_SLICE && T > kChainNarrowMaxT && tiles < kChainMinTiles) return false;
+  if (c.form == DEAMOE_FORM_SLICE && tiles < kChainMinTiles &&
+      T > (tiles >= kChainNarrowMinTiles ? kChainNarrowMaxT : 4))
+    return false;
   const int dk = std::min(c.top_k_dept > 0 ? c.top_k_dept : c.top_k, std::min(c.top_k, c.n_depts));
   const bool slice_priv = c.form == DEAMOE_FORM_SLICE && c.d_private > 0;
   const int units = std::min(c.n_depts, T * dk) +
@@ -551,8 +565,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
                                    factored_priv_ks_of(c, T), tiles_bound(act_exps, d) * groups,
                                    kGridCap, s));
     DEAMOE_TRY(ev.mark());
-    DEAMOE_TRY(launch_down(stage(2), wt, ntt, groups, down_ks_of(c, T), act_exps, d,
-                           kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(2), wt, down_ntt_of(c, T), down_groups_max(c, T),
+                           down_ks_of(c, T), act_exps, d, kGridCap, s));
     DEAMOE_TRY(ev.mark());
     ZsumArgs za;
     za.counts = pc;
@@ -583,8 +597,8 @@ int layer_impl(const deamoe_config *cfg, int32_t T, const void *x, const deamoe_
       DEAMOE_TRY(ev.mark());
       return DEAMOE_OK;
     }
-    DEAMOE_TRY(launch_down(stage(3), wt, ntt, groups, down_ks_of(c, T), act_depts + se,
-                           c.hidden, kGridCap, s));
+    DEAMOE_TRY(launch_down(stage(3), wt, down_ntt_of(c, T), down_groups_max(c, T),
+                           down_ks_of(c, T), act_depts + se, c.hidden, kGridCap, s));
     DEAMOE_TRY(ev.mark());
   }
   CombineArgs ca;
