@@ -172,19 +172,22 @@ int ntt_of(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : T <= 64 ? 4 : 8; }
 // Token tiles per wave in the gate/up stage.  A unit with more tokens than
 // one wave holds gets one work item per token group, and every group
 // streams the unit's rows.  SLICE: one tile up to 16 tokens, two above, and
-// four above 96 tokens on layers at least 4096 wide.  Same-process A/B, us
-// per step, two tiles -> four, outputs bit-identical: the DeepSeek-V3 shape
-// 1005.7 -> 973.9 at 128 tokens (900.0 -> 897.3 at 96), fp8 651.7 -> 635.8
-// at 128 (563.9 -> 569.1 at 96), skewed routing 500.9 -> 499.4 at 128
-// (436.3 -> 439.5 at 96); the 2048-wide 7B-class layer 145.8 -> 153.1 at
-// 128, where four tiles halve its work items and leave the three-wave
-// two-tile kernel for a two-wave one.  The FACTORED stages keep one tile at
+// on layers at least 4096 wide four above 64 tokens (fp8: above 96).
+// Same-process A/B, us per step, two tiles -> four, outputs bit-identical,
+// with the token rows loaded as whole segments: the DeepSeek-V3 shape 950.2
+// -> 917.3 at 128 tokens, 868.4 -> 864.8 at 96, 818.8 -> 818.1 at 72;
+// skewed routing 463.2 -> 447.2 at 128, 412.7 -> 402.7 at 96, 369.1 ->
+// 363.3 at 72; fp8 645.3 -> 631.1 at 128 but 515.8 -> 531.2 at 96 and 477.2
+// -> 489.3 at 72.  The 2048-wide 7B-class layer was slower with four
+// (145.8 -> 153.1 at 128, before the whole-segment rows): they halve its
+// work items and leave the three-wave two-tile kernel for a two-wave one.  The FACTORED stages keep one tile at
 // every batch: its private gate/up then runs at three waves per SIMD, which
 // outweighs streaming the rows of a unit with more than 16 tokens once per
 // group.
 int wave_ntt_of(const deamoe_config &c, int T) {
   if (c.form == DEAMOE_FORM_FACTORED) return 1;
-  return T <= kTile ? 1 : T <= 96 || c.hidden < 4096 ? 2 : 4;
+  const int four_from = c.w_dtype == DEAMOE_FP8_E4M3_B128 ? 97 : 65;
+  return T <= kTile ? 1 : T < four_from || c.hidden < 4096 ? 2 : 4;
 }
 int token_groups_max(const deamoe_config &c, int T) {
   const int gt = kTile * wave_ntt_of(c, T);

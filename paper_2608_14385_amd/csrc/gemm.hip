@@ -71,8 +71,8 @@ void grouped_gemm_occ3_kernel(GemmStage st) {
 }
 
 // Four token tiles per wave (64 tokens), for the gate/up stage of wide
-// layers above 96 tokens: a unit with many tokens streams its rows once per
-// 64 tokens instead of once per 32.  The token operand is requested per step (B1);
+// layers above 64 tokens (fp8: above 96): a unit with many tokens streams
+// its rows once per 64 tokens instead of once per 32.  The token operand is requested per step (B1);
 // two waves per SIMD.
 template <int WT, int NW, int NTT, int KS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))

@@ -152,7 +152,7 @@ def test_fused_down_combine(variant):
 
 @pytest.mark.parametrize("variant", ["f32_t128_se", "bf16_t128_se"])
 def test_four_token_tiles(variant):
-    """Above 96 tokens on layers at least 4096 wide the gate/up stage holds
+    """Above 64 tokens on layers at least 4096 wide the gate/up stage holds
     four token tiles per wave: 128 tokens, top-4 over 4 departments, so each
     department has 84-104 tokens in two token groups of 64 (the second one
     ragged) and the shared expert two full ones; fp32 weights (the operand
