@@ -194,13 +194,15 @@ int token_groups_max(const deamoe_config &c, int T) {
   return (T + gt - 1) / gt;
 }
 // Token tiles per wave in the separate down stages (above 32 tokens for
-// SLICE).  Layers narrower than 4096 keep one tile up to 64 tokens: there
+// SLICE).  Layers narrower than 4096 keep one tile up to 56 tokens: there
 // the one-tile row pairs at three waves per SIMD outweigh streaming the rows
-// of a unit with more than 16 tokens once per group (same-process A/B, us
-// per step, one tile -> two: the 7B-class layer 89.4 -> 104.3 at 48 tokens,
-// 106.2 -> 110.5 at 64).  Wider layers take two (the DeepSeek-V3 shape
-// 776.5 -> 775.3 at 56, 819.6 -> 806.3 at 64; fp8 482.7 -> 480.4 and skewed
-// routing 368.5 -> 361.5 at 64; even at 48).
+// of a unit with more than 16 tokens once per group (same-process A/B with
+// the token rows loaded as whole segments, us per step, one tile -> two: the
+// 7B-class layer 84.0 -> 91.3 at 40 tokens, 85.3 -> 92.2 at 52, 87.9 ->
+// 92.9 at 56, but 96.3 -> 94.2 at 60 and 98.9 -> 96.9 at 64; before those
+// rows two tiles lost at 64 too, 106.2 -> 110.5).  Wider layers take two
+// (the DeepSeek-V3 shape 776.5 -> 775.3 at 56, 819.6 -> 806.3 at 64; fp8
+// 482.7 -> 480.4 and skewed routing 368.5 -> 361.5 at 64; even at 48).
 // Row pairs hold at most two token tiles.  The FACTORED down stages (the
 // private B_e and the department W_d^T) take two from 17 tokens on layers at
 // least 4096 wide, where a department's W_d^T then streams once per 32
@@ -211,7 +213,7 @@ int token_groups_max(const deamoe_config &c, int T) {
 // the 1024-wide Baseline-7B layer was slower (120.6 -> 124.3 at 64).
 int down_ntt_of(const deamoe_config &c, int T) {
   if (c.form == DEAMOE_FORM_FACTORED) return T > kTile && c.hidden >= 4096 ? 2 : 1;
-  return c.form == DEAMOE_FORM_SLICE && T <= 64 && c.hidden < 4096 ? 1
+  return c.form == DEAMOE_FORM_SLICE && T <= 56 && c.hidden < 4096 ? 1
                                                                      : std::min(2, wave_ntt_of(c, T));
 }
 int down_groups_max(const deamoe_config &c, int T) {
