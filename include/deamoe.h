@@ -78,6 +78,10 @@ extern "C" {
 #define DEAMOE_MAX_TOKENS 128
 #define DEAMOE_MAX_EXPERTS 2048
 #define DEAMOE_MAX_TOPK 32
+/* every width (hidden, d_shared, d_private, d_shared_expert) is at most this
+ * many columns, so that the token rows one stage reads lie within 4 GiB of
+ * their buffer (32-bit row offsets in the expert stages) */
+#define DEAMOE_MAX_WIDTH 65536
 /* fp8 weights: every contraction length (hidden, d_shared, d_private,
  * d_shared_expert) is at most this many columns (64 scale blocks) */
 #define DEAMOE_MAX_FP8_K 8192

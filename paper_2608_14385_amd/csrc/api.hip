@@ -135,6 +135,9 @@ int validate_config(const deamoe_config *c) {
       c->top_k > DEAMOE_MAX_TOPK || c->n_depts > kMaxM)
     return DEAMOE_ERR_UNSUPPORTED;
   if (c->top_k_dept > 0 && c->n_depts > kMaxMGrouped) return DEAMOE_ERR_UNSUPPORTED;
+  if (c->hidden > DEAMOE_MAX_WIDTH || c->d_shared > DEAMOE_MAX_WIDTH ||
+      c->d_private > DEAMOE_MAX_WIDTH || c->d_shared_expert > DEAMOE_MAX_WIDTH)
+    return DEAMOE_ERR_UNSUPPORTED;
   // fp32 weights pair with fp32 activations, bf16 / fp8 weights with bf16
   if ((c->w_dtype == DEAMOE_F32) != (c->act_dtype == DEAMOE_F32)) return DEAMOE_ERR_UNSUPPORTED;
   // every contraction length is a whole number of matrix-core K steps

@@ -266,7 +266,13 @@ __device__ inline void tile_loop(const GemmUnit &U, int rt0, int nsub, int kp, i
   using LB = WLoad<WT_BF16>;   // token rows are bf16
   static_assert(!ROWS || (ASEG == LB::WSEG && LB::NQ == 4 && NW * LD::REGION >= LB::REGION),
                 "a token tile is staged like one bf16 weight tile");
-  uint32_t boffs[ROWS ? NTT : 1][4];   // byte offsets from in0 of the rows this lane loads
+  // byte offsets from in0 of the rows this lane loads: below 2^32, as a stage
+  // reads at most one row per (token, selected expert) pair, of at most
+  // DEAMOE_MAX_WIDTH bf16 columns
+  static_assert((int64_t)DEAMOE_MAX_TOKENS * DEAMOE_MAX_TOPK * DEAMOE_MAX_WIDTH * 2 <
+                    (int64_t{1} << 32),
+                "32-bit row offsets");
+  uint32_t boffs[ROWS ? NTT : 1][4];
   if constexpr (ROWS) {
 #pragma unroll
     for (int tt = 0; tt < NTT; ++tt)

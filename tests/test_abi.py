@@ -71,6 +71,8 @@ def ws_status(c):
     (dict(w_dtype="f32"), D.ERR_UNSUPPORTED),                # fp32 weights with bf16 activations
     (dict(n_experts=4096, n_depts=32), D.ERR_UNSUPPORTED),
     (dict(top_k=40), D.ERR_UNSUPPORTED),
+    (dict(hidden=65536 + 128), D.ERR_UNSUPPORTED),           # beyond DEAMOE_MAX_WIDTH
+    (dict(d_shared=65536 + 128), D.ERR_UNSUPPORTED),
     (dict(top_k_dept=4, dept_cover=1), D.OK),
     (dict(dept_cover=1), D.ERR_INVALID),                     # strict coverage needs top_k_dept > 0
     (dict(top_k_dept=9, n_depts=32, top_k=8, dept_cover=1), D.ERR_INVALID),   # k < k_dept
