@@ -39,9 +39,9 @@ HBM_PEAK_GBPS = 8000.0
 #  - the average launch duration from a kernel-trace run of the default
 #    command (profiles/gate_up_dsv3_bf16_T16_kernel_trace.md), which excludes
 #    the launch gap that the benchmark's own events include.
-TRAFFIC_BYTES = 2341137408
-PROFILED_GATE_UP_US = 337.93
-TRAFFIC_SOURCES_SHA256 = "542a5d73c69d28d32c1765d3348911d49903c03953028c4a10400c5bb19de0f7"
+TRAFFIC_BYTES = 2341137203
+PROFILED_GATE_UP_US = 338.51
+TRAFFIC_SOURCES_SHA256 = "a515ca9f903cc2dd2c3cf5ca88186bb380712a58e6698ae2821975486be73e76"
 
 
 def library_sources_digest() -> str:
