@@ -206,7 +206,12 @@ int token_groups_max(const deamoe_config &c, int T) {
 // rows two tiles lost at 64 too, 106.2 -> 110.5).  Wider layers take two
 // (the DeepSeek-V3 shape 776.5 -> 775.3 at 56, 819.6 -> 806.3 at 64; fp8
 // 482.7 -> 480.4 and skewed routing 368.5 -> 361.5 at 64; even at 48).
-// Row pairs hold at most two token tiles.  The FACTORED down stages (the
+// Where the gate/up stage takes four token tiles, the bf16 down stage takes
+// four too (row pairs of 64 tokens, two waves per SIMD): same-process A/B,
+// us per step, outputs bit-identical: skewed routing 363.2 -> 353.6 at 72
+// tokens, 402.5 -> 393.4 at 96, 447.6 -> 437.8 at 128; the DeepSeek-V3
+// shape 817.5 -> 815.3 at 72, 919.3 -> 907.7 at 128.  fp8 keeps two (569.9
+// -> 581.2 at 128 with four).  The FACTORED down stages (the
 // private B_e and the department W_d^T) take two from 17 tokens on layers at
 // least 4096 wide, where a department's W_d^T then streams once per 32
 // tokens instead of once per 16 (same-process A/B, us per step, outputs
@@ -216,8 +221,9 @@ int token_groups_max(const deamoe_config &c, int T) {
 // the 1024-wide Baseline-7B layer was slower (120.6 -> 124.3 at 64).
 int down_ntt_of(const deamoe_config &c, int T) {
   if (c.form == DEAMOE_FORM_FACTORED) return T > kTile && c.hidden >= 4096 ? 2 : 1;
-  return c.form == DEAMOE_FORM_SLICE && T <= 56 && c.hidden < 4096 ? 1
-                                                                     : std::min(2, wave_ntt_of(c, T));
+  if (c.form == DEAMOE_FORM_SLICE && T <= 56 && c.hidden < 4096) return 1;
+  const int n = wave_ntt_of(c, T);
+  return c.w_dtype == DEAMOE_FP8_E4M3_B128 ? std::min(2, n) : n;
 }
 int down_groups_max(const deamoe_config &c, int T) {
   const int gt = kTile * down_ntt_of(c, T);

@@ -71,13 +71,14 @@ void grouped_gemm_occ3_kernel(GemmStage st) {
 }
 
 // Four token tiles per wave (64 tokens), for the gate/up stage of wide
-// layers above 64 tokens (fp8: above 96): a unit with many tokens streams
-// its rows once per 64 tokens instead of once per 32.  The token operand is requested per step (B1);
+// layers above 64 tokens (fp8: above 96) and the bf16 down stage's row pairs
+// there: a unit with many tokens streams its rows once per 64 tokens instead
+// of once per 32.  The token operand is requested per step (B1);
 // two waves per SIMD.
-template <int WT, int NW, int NTT, int KS>
+template <int WT, int NW, int NTT, int KS, bool PAIR>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void grouped_gemm_wide_kernel(GemmStage st) {
-  grouped_gemm_body<WT, NW, NTT, KS, false, false, true>(st);
+  grouped_gemm_body<WT, NW, NTT, KS, false, PAIR, true>(st);
 }
 
 // mode: GemmMode; row pairs exist for NTT <= 2 only (the host picks them so).
@@ -93,9 +94,13 @@ static hipError_t launch_gemm(const GemmStage &st, int mode, int max_tiles, int 
     hipLaunchKernelGGL(k, dim3(grid), dim3(256), 0, s, st);
     return hipGetLastError();
   };
-  if constexpr (NTT == 4) {   // four tiles: two-matrix gate/up tiles only
-    if (mode != GEMM_PLAIN) return hipErrorInvalidValue;
-    return plain(grouped_gemm_wide_kernel<WT, NW, NTT, KS>);
+  if constexpr (NTT == 4) {   // four tiles: gate/up with a two-wave K split, row pairs without
+    if constexpr (KS == 2) {
+      if (mode == GEMM_PLAIN) return plain(grouped_gemm_wide_kernel<WT, NW, NTT, KS, false>);
+    } else if constexpr (KS == 1 && WT != WT_FP8) {
+      if (mode == GEMM_PAIR) return plain(grouped_gemm_wide_kernel<WT, NW, NTT, KS, true>);
+    }
+    return hipErrorInvalidValue;
   }
   if constexpr (NW == 2) {
     if (mode == GEMM_SPLIT) {
@@ -129,8 +134,8 @@ static hipError_t dispatch_ntt(const GemmStage &st, int mode, int ntt, int max_t
   switch (ntt) {
     case 1: return launch_gemm<WT, NW, 1, KS>(st, mode, max_tiles, cap, narrow, s);
     case 2: return launch_gemm<WT, NW, 2, KS>(st, mode, max_tiles, cap, narrow, s);
-    case 4:
-      if constexpr (KS == 2) return launch_gemm<WT, NW, 4, KS>(st, mode, max_tiles, cap, narrow, s);
+    case 4:   // gate/up with a K split over 2 waves, row pairs without one
+      if constexpr (KS <= 2) return launch_gemm<WT, NW, 4, KS>(st, mode, max_tiles, cap, narrow, s);
       return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
