@@ -39,9 +39,9 @@ HBM_PEAK_GBPS = 8000.0
 #  - the average launch duration from a kernel-trace run of the default
 #    command (profiles/gate_up_dsv3_bf16_T16_kernel_trace.md), which excludes
 #    the launch gap that the benchmark's own events include.
-TRAFFIC_BYTES = 2341137203
-PROFILED_GATE_UP_US = 338.51
-TRAFFIC_SOURCES_SHA256 = "a515ca9f903cc2dd2c3cf5ca88186bb380712a58e6698ae2821975486be73e76"
+TRAFFIC_BYTES = 2341123891
+PROFILED_GATE_UP_US = 339.79
+TRAFFIC_SOURCES_SHA256 = "361aea0906084eeb101d19129b97a0c402923f153d07bc7453aa965256e73f91"
 
 
 def library_sources_digest() -> str:
