@@ -84,7 +84,7 @@ void small_route_gate_up_kernel(RouteArgs a) {
   __shared__ SmallSmem ps;
   __shared__ int32_t s_idx[kSmallT][kSmallT];   // per wave: member tokens of its unit
   TokSmem *tsm = lds.tsm;
-  const int wave = uniform(threadIdx.x / kWave), lane = lane_id(), tid = threadIdx.x;
+  const int wave = uniform(threadIdx.x / kWave), lane = lane_id();
   const bool planner = blockIdx.x == 0;
   const int T = a.T, m = a.m, n = a.n;
   const int dwords = (m + 31) / 32, ewords = (n + 31) / 32;
