@@ -40,8 +40,8 @@ HBM_PEAK_GBPS = 8000.0
 #    command (profiles/gate_up_dsv3_bf16_T16_kernel_trace.md), which excludes
 #    the launch gap that the benchmark's own events include.
 TRAFFIC_BYTES = 2341123891
-PROFILED_GATE_UP_US = 339.79
-TRAFFIC_SOURCES_SHA256 = "361aea0906084eeb101d19129b97a0c402923f153d07bc7453aa965256e73f91"
+PROFILED_GATE_UP_US = 339.66
+TRAFFIC_SOURCES_SHA256 = "642b1e82bc6283e4a1c664beac1f39abd57d15368ba13a966b2f9276ae23cdce"
 
 
 def library_sources_digest() -> str:
